@@ -1,0 +1,244 @@
+"""fp64 CPU oracle for the BaKron solver -- TEST INFRASTRUCTURE ONLY.
+
+Only ``tests/``, ``__graft_entry__.smoke()`` and ``bench.py``'s cpu_baseline leg
+may import this module.  It shares no code with the HIP solver in
+``paper_2608_06291_amd/``; neither imports the other.
+
+Contents, each following a passage of arXiv 2608.06291:
+
+* :func:`damp` -- regularisation: add a multiple of the mean diagonal to the
+  diagonal (Sec. 4 opening; App. D uses 0.5, the workloads here use 0.01).
+* :func:`normalized_factor` -- ``Cholesky(X^-1)`` with every column divided by
+  its diagonal entry (Alg. 1 / Alg. 2, first two lines).  Literal route:
+  explicit inverse, then Cholesky (LAPACK via numpy, fp64).
+* :func:`babai` -- the sequential rounding itself: Alg. 2 (BaKron-naive) in C
+  (``babai.c``), optionally tie-forced.
+* :func:`ar1_diffusion` -- exact O(mn) special case for AR(1) Toeplitz A, B.
+* :func:`rev_cholesky` / :func:`certificate` -- closed-form check of any
+  candidate output: by Eq. (1) the final workspace is
+  ``V = W0 + L^B E (L^A)^T``, so ``E = R^_B (V - W0) R^_A^T`` with
+  ``R^_X = (L^X)^-1`` = RevCholesky(X) with rows divided by their diagonal
+  (Sec. 3.1 definition of RevCholesky), and the pre-rounding values are
+  ``W~ = V - E``.  V is a valid sequential-rounding output iff
+  ``V = quantise(W~)`` entrywise up to ties.
+* :func:`objective` -- ``tr((W - V)^T B (W - V) A)``, which equals
+  ``vec(W - V)^T (A (x) B) vec(W - V)`` by Prop. 3.1.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "babai.c")
+_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+_lib = None
+
+
+def build(force: bool = True) -> str:
+    """Compile babai.c into liboracle.so with gcc (plain C, -O2, no fast-math)."""
+    if force or not os.path.exists(_LIB_PATH):
+        tmp = _LIB_PATH + ".tmp"
+        subprocess.check_call(
+            ["gcc", "-O2", "-std=c99", "-fPIC", "-shared", "-fno-fast-math",
+             "-o", tmp, _SRC, "-lm"])
+        os.replace(tmp, _LIB_PATH)
+    return _LIB_PATH
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB_PATH):
+            build(force=True)
+        lib = ctypes.CDLL(_LIB_PATH)
+        dp = ctypes.POINTER(ctypes.c_double)
+        i8p = ctypes.POINTER(ctypes.c_int8)
+        i64p = ctypes.POINTER(ctypes.c_int64)
+        lib.oracle_babai_naive.restype = ctypes.c_int
+        lib.oracle_babai_naive.argtypes = [
+            ctypes.c_int64, ctypes.c_int64, dp, dp, dp, dp, ctypes.c_int,
+            i8p, ctypes.c_double, i8p, dp, dp, i64p, i64p]
+        lib.oracle_ar1_diffusion.restype = ctypes.c_int
+        lib.oracle_ar1_diffusion.argtypes = [
+            ctypes.c_int64, ctypes.c_int64, dp, ctypes.c_double, ctypes.c_double,
+            dp, ctypes.c_int, i8p, dp, dp]
+        _lib = lib
+    return _lib
+
+
+def _dptr(a):
+    return a.ctypes.data_as(ctypes.POINTER(ctypes.c_double))
+
+
+def _i8ptr(a):
+    return a.ctypes.data_as(ctypes.POINTER(ctypes.c_int8))
+
+
+def qmax_of_bits(bits: int) -> int:
+    """Symmetric alphabet {-l..l} with l = 2^(bits-1) - 1 (App. D uses l = 3)."""
+    return (1 << (int(bits) - 1)) - 1
+
+
+def damp(X, lam: float) -> np.ndarray:
+    """X + lam * mean(diag X) * I in fp64 (Sec. 4 opening, App. D)."""
+    X = np.asarray(X, dtype=np.float64)
+    d = X.shape[0]
+    out = X.copy()
+    out[np.diag_indices(d)] += float(lam) * float(np.mean(np.diag(X)))
+    return out
+
+
+def normalized_factor(X, lam: float) -> np.ndarray:
+    """Unit-lower L = Cholesky(X_d^-1) with column j divided by L_jj (Alg. 2)."""
+    Xd = damp(X, lam)
+    Linv = np.linalg.cholesky(np.linalg.inv(Xd))
+    return Linv / np.diag(Linv)[None, :]
+
+
+def rev_cholesky(Xd) -> np.ndarray:
+    """Lower R with positive diagonal and R^T R = Xd (Sec. 3.1 definition).
+
+    With P the reversal permutation, P Xd P = C C^T gives R = P C^T P.
+    """
+    Xd = np.asarray(Xd, dtype=np.float64)
+    C = np.linalg.cholesky(Xd[::-1, ::-1])
+    return np.ascontiguousarray(C[::-1, ::-1].T)
+
+
+def babai(W, LA, LB, scale, bits: int, forced=None, tie_window: float = 0.0):
+    """Sequential rounding of Alg. 2 (row-major), in C.  Returns a dict with
+    codes (int8), V (fp64), pre (x = W~/s, fp64), n_excused, n_flip."""
+    lib = _load()
+    W = np.ascontiguousarray(W, dtype=np.float64)
+    m, n = W.shape
+    LA = np.ascontiguousarray(LA, dtype=np.float64)
+    LB = np.ascontiguousarray(LB, dtype=np.float64)
+    s = np.ascontiguousarray(scale, dtype=np.float64).reshape(m)
+    assert LA.shape == (n, n) and LB.shape == (m, m)
+    codes = np.zeros((m, n), np.int8)
+    V = np.zeros((m, n), np.float64)
+    pre = np.zeros((m, n), np.float64)
+    exc = ctypes.c_int64(0)
+    flip = ctypes.c_int64(0)
+    fp = None
+    if forced is not None:
+        forced = np.ascontiguousarray(forced, dtype=np.int8)
+        assert forced.shape == (m, n)
+        fp = _i8ptr(forced)
+    rc = lib.oracle_babai_naive(m, n, _dptr(W), _dptr(LA), _dptr(LB), _dptr(s),
+                                qmax_of_bits(bits), fp, float(tie_window),
+                                _i8ptr(codes), _dptr(V), _dptr(pre),
+                                ctypes.byref(exc), ctypes.byref(flip))
+    if rc != 0:
+        raise MemoryError("oracle_babai_naive: allocation failed")
+    return dict(codes=codes, V=V, pre=pre, n_excused=int(exc.value),
+                n_flip=int(flip.value))
+
+
+def solve(W, A, B, damp_lambda: float, scale, bits: int, forced=None,
+          tie_window: float = 0.0):
+    """Factors by the literal route, then :func:`babai`.  B=None means I_m."""
+    W = np.asarray(W, dtype=np.float64)
+    m, n = W.shape
+    LA = normalized_factor(A, damp_lambda)
+    LB = np.eye(m) if B is None else normalized_factor(B, damp_lambda)
+    return babai(W, LA, LB, scale, bits, forced=forced, tie_window=tie_window)
+
+
+def ar1_diffusion(W, rhoA: float, rhoB: float, scale, bits: int):
+    """Exact output for A = [rhoA^|i-j|], B = [rhoB^|i-j|] without damping."""
+    lib = _load()
+    W = np.ascontiguousarray(W, dtype=np.float64)
+    m, n = W.shape
+    s = np.ascontiguousarray(scale, dtype=np.float64).reshape(m)
+    codes = np.zeros((m, n), np.int8)
+    V = np.zeros((m, n), np.float64)
+    pre = np.zeros((m, n), np.float64)
+    rc = lib.oracle_ar1_diffusion(m, n, _dptr(W), float(rhoA), float(rhoB), _dptr(s),
+                                  qmax_of_bits(bits), _i8ptr(codes), _dptr(V), _dptr(pre))
+    if rc != 0:
+        raise MemoryError("oracle_ar1_diffusion: allocation failed")
+    return dict(codes=codes, V=V, pre=pre)
+
+
+def near_boundary(x, bits: int, window: float) -> np.ndarray:
+    """Entries whose grid value x lies within `window` of a boundary k+1/2,
+    k in [-l, l-1]; NaN (zero-scale rows) is never near a boundary."""
+    l = qmax_of_bits(bits)
+    x = np.asarray(x, dtype=np.float64)
+    k = np.floor(x)
+    with np.errstate(invalid="ignore"):
+        near = (np.abs(x - (k + 0.5)) < window) & (k >= -l) & (k <= l - 1)
+    return near & np.isfinite(x)
+
+
+def quantise_codes(x, bits: int) -> np.ndarray:
+    """clamp(rint(float32(x)), -l, l); NaN (zero scale) maps to 0."""
+    l = qmax_of_bits(bits)
+    xf = np.asarray(x, dtype=np.float64).astype(np.float32)
+    with np.errstate(invalid="ignore"):
+        c = np.clip(np.rint(xf), -l, l)
+    c = np.where(np.isfinite(xf), c, 0)
+    return c.astype(np.int8)
+
+
+def certificate(W, A, B, damp_lambda: float, scale, codes, bits: int,
+                rows=None, RA=None, RB=None):
+    """Pre-rounding values implied by a candidate output (closed form).
+
+    Returns x = W~/s for the requested rows (all rows if None), computed as
+    W~ = V - R^_B (V - W0) R^_A^T with V = s_i * codes in fp64.  RA/RB may
+    pass precomputed RevCholesky factors of the damped matrices.
+    """
+    W = np.asarray(W, dtype=np.float64)
+    m, n = W.shape
+    s = np.asarray(scale, dtype=np.float64).reshape(m)
+    V = s[:, None] * np.asarray(codes, dtype=np.float64)
+    if RA is None:
+        RA = rev_cholesky(damp(A, damp_lambda))
+    if B is None:
+        RB = np.eye(m)
+    elif RB is None:
+        RB = rev_cholesky(damp(B, damp_lambda))
+    RhA = RA / np.diag(RA)[:, None]
+    RhB = RB / np.diag(RB)[:, None]
+    D = V - W
+    if rows is None:
+        E = RhB @ D @ RhA.T
+        Vr = V
+    else:
+        rows = np.asarray(rows)
+        E = (RhB[rows, :] @ D) @ RhA.T
+        Vr = V[rows]
+    Wt = Vr - E
+    sr = s if rows is None else s[rows]
+    with np.errstate(divide="ignore", invalid="ignore"):
+        x = Wt / sr[:, None]
+    x[sr == 0.0, :] = np.nan
+    return x
+
+
+def verdict(codes, x, bits: int, window: float = 1e-4):
+    """Compare candidate codes with quantise(x) along the candidate's own
+    trajectory.  violations: differ and not near a boundary (must be 0);
+    flips: differ at near-boundary entries (excused, rate-limited)."""
+    codes = np.asarray(codes)
+    own = quantise_codes(x, bits)
+    near = near_boundary(x, bits, window)
+    diff = own != codes
+    return dict(violations=int(np.count_nonzero(diff & ~near)),
+                flips=int(np.count_nonzero(diff & near)),
+                near=int(np.count_nonzero(near)),
+                total=int(codes.size))
+
+
+def objective(W, V, A, B, damp_lambda: float) -> float:
+    """tr((W - V)^T B_d (W - V) A_d) in fp64 with the damped factors."""
+    D = np.asarray(W, dtype=np.float64) - np.asarray(V, dtype=np.float64)
+    Ad = damp(A, damp_lambda)
+    BD = D if B is None else damp(B, damp_lambda) @ D
+    return float(np.sum(BD * (D @ Ad)))
