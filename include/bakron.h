@@ -1,0 +1,160 @@
+/*
+ * bakron.h -- C ABI of libbakron.so, an MI355X (gfx950) solver for BaKron
+ * (arXiv 2608.06291): sequential Babai / GPTQ rounding of an m x n weight
+ * matrix W under a Kronecker-factored Hessian A (x) B (A: n x n acting on the
+ * input/column side, B: m x m acting on the output/row side).
+ *
+ * Problem statement (Sec. 3.2, Alg. 2; Alg. 6 is the solver; Thm 3.2 states
+ * that all variants return the same output): given W, A, B, return the
+ * quantised V obtained by visiting the entries in any order compatible with
+ * "(i,j) before (p,q) whenever i<=p and j<=q", quantising each entry at its
+ * current value, and feeding the error back to the later entries through
+ * the unit-lower factors L^A = normalised Cholesky(A^-1) and
+ * L^B = normalised Cholesky(B^-1).  "round" is replaced by quantisation to
+ * the symmetric alphabet {-l..l}, l = 2^(bits-1) - 1, with a per-row scale
+ * (Sec. 3.1; App. D), ties to even.
+ *
+ * Conventions for every entry point:
+ *   - All matrices are row-major, contiguous, fp32 unless stated otherwise.
+ *   - Pointers marked "device" must be HIP device (or managed) memory on the
+ *     device current at the call; the library never frees caller memory.
+ *   - Errors found on the host (null pointers, bad sizes, bad bits, shape
+ *     mismatch with the factor handle) return BAKRON_EINVAL before any work
+ *     is enqueued.  HIP runtime failures return BAKRON_EHIP.  Allocation
+ *     failures return BAKRON_ENOMEM.
+ *   - Not thread-safe per handle: one solve at a time per bakron_factors
+ *     (the handle owns the solve workspace).
+ */
+#ifndef BAKRON_H
+#define BAKRON_H
+
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    BAKRON_OK = 0,
+    BAKRON_EINVAL = 1,   /* invalid argument (host-side validation)            */
+    BAKRON_ENOTSPD = 2,  /* a damped factor matrix is not positive definite    */
+    BAKRON_ENOMEM = 3,   /* device or host allocation failed                   */
+    BAKRON_EHIP = 4      /* a HIP runtime call failed                          */
+} bakron_status;
+
+/* Opaque, library-owned, device-resident: the two normalised factors in
+ * fp32 plus the cached solve workspace for the last (m, n) solved. */
+typedef struct bakron_factors bakron_factors;
+
+/* Quantiser (Sec. 3.1; App. D): alphabet {-l..l} with l = 2^(bits-1) - 1,
+ * bits in [2, 8]; scale is a DEVICE pointer to m fp32 per-row scales
+ * s_i >= 0 (s_i = 0 means the row's alphabet is {0}).  The caller chooses
+ * the scales (App. D uses max_j |W_ij| / l). */
+typedef struct {
+    int32_t bits;
+    const float *scale;
+} bakron_quantizer;
+
+/*
+ * bakron_factor -- damp and factor the Kronecker factors once (App. B: the
+ * factorisations are done only at the top level).
+ *
+ *   A     device, n x n, symmetric positive semi-definite (undamped Gram)
+ *   n     > 0
+ *   B     device, m x m, symmetric PSD, or NULL for B = I_m (one-sided
+ *         GPTQ, Sec. 1); then m may be any value and is not checked
+ *   m     > 0 when B != NULL
+ *   damp  >= 0, finite: X <- X + damp * mean(diag X) * I, each matrix with
+ *         its own mean diagonal (Sec. 4 opening; App. D)
+ *   stream  HIP stream for all work (0 = default stream)
+ *   out   receives the handle on BAKRON_OK; untouched otherwise
+ *
+ * Computes, in fp64 on the device, L^X = R_X^-1 diag(R_X) where
+ * R_X = RevCholesky(X_d) (Sec. 3.1 definition); this equals the normalised
+ * Cholesky(X_d^-1) of Alg. 2.  The fp32 result is kept in the handle.
+ * Synchronises `stream` once to report BAKRON_ENOTSPD (a non-positive or
+ * non-finite pivot); bakron_factors_error() then names the matrix and pivot.
+ */
+bakron_status bakron_factor(const float *A, int64_t n, const float *B, int64_t m,
+                            float damp, hipStream_t stream, bakron_factors **out);
+
+/*
+ * bakron_solve -- the BaKron rounding (Alg. 6), asynchronous on `stream`.
+ *
+ *   W      device, m x n, not modified
+ *   m, n   must equal the handle's sizes (n always; m when B was given)
+ *   f      handle from bakron_factor
+ *   q      quantiser; q.scale is a device pointer to m floats
+ *   codes  device, m x n int8 output in [-l, l]
+ *   V      device, m x n fp32 output, V_ij = s_i * codes_ij (one fp32 product)
+ *
+ * The first call for a given (m, n) allocates the workspace (about 8*m*n
+ * bytes) and builds the launch schedule; later calls with the same (m, n)
+ * allocate nothing and never synchronise the host.  Kernel faults surface as
+ * BAKRON_EHIP on a later call or at the caller's synchronisation.
+ */
+bakron_status bakron_solve(const float *W, int64_t m, int64_t n, const bakron_factors *f,
+                           bakron_quantizer q, int8_t *codes, float *V, hipStream_t stream);
+
+/*
+ * bakron_solve_debug -- bakron_solve that also writes, for every entry, the
+ * pre-rounding value in grid units x_ij = W~_ij / s_i (device, m x n fp32;
+ * NaN on zero-scale rows), the value at which the entry was quantised.
+ * Used to measure the numerical margin against the fp64 oracle.
+ */
+bakron_status bakron_solve_debug(const float *W, int64_t m, int64_t n, const bakron_factors *f,
+                                 bakron_quantizer q, int8_t *codes, float *V, float *pre,
+                                 hipStream_t stream);
+
+/* Frees the handle, its factors and its workspace (synchronises the device
+ * work that used them).  NULL is a no-op. */
+void bakron_factors_free(bakron_factors *f);
+
+/* Static, never NULL. */
+const char *bakron_status_string(bakron_status s);
+
+/* Last error message recorded on the handle ("" if none); valid until the
+ * next call on the handle. */
+const char *bakron_factors_error(const bakron_factors *f);
+
+/* Message of the last failed bakron_factor call in this thread ("" if none). */
+const char *bakron_last_error(void);
+
+/*
+ * bakron_factor_export -- copy a normalised factor out of the handle as a
+ * dense row-major fp32 matrix (which = 0: L^A, n x n; which = 1: L^B, m x m).
+ * dst is a device pointer.  Asynchronous on `stream`.  For testing.
+ */
+bakron_status bakron_factor_export(const bakron_factors *f, int which, float *dst,
+                                   hipStream_t stream);
+
+/*
+ * Measurement hook (not needed for solving).  While enabled, every
+ * bakron_solve on the handle records a HIP event pair on its stream around
+ * each kernel launch (which adds a few microseconds per launch).  After the
+ * caller has synchronised that stream, bakron_profile_read returns, for the
+ * last profiled solve, per kernel class:
+ *   ms          summed launch durations
+ *   launches    number of launches
+ *   flops       algorithmic work: 2*32^3 flops per (source, target) tile pair
+ *               fed back (Eq. (1)), plus the in-tile pairs of the leaves;
+ *               for the prep class, bytes moved instead
+ *   mfma_flops  flops executed on the matrix cores, zero-masked tiles included
+ * Returns BAKRON_EINVAL if no profiled solve has been enqueued since enabling.
+ */
+typedef struct {
+    double ms;
+    int64_t launches;
+    double flops;
+    double mfma_flops;
+} bakron_kernel_stat;
+
+bakron_status bakron_profile_enable(bakron_factors *f, int on);
+bakron_status bakron_profile_read(const bakron_factors *f, bakron_kernel_stat *prep,
+                                  bakron_kernel_stat *leaf, bakron_kernel_stat *node);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* BAKRON_H */

@@ -63,11 +63,14 @@ static int near_boundary(double x, int qmax, double window)
  *   forced: NULL, or m x n codes to adopt at near-boundary entries
  * Outputs: codes (m x n), V = s_i * code (m x n), pre = x = W~/s (m x n; NaN
  * for zero-scale rows), counters.  Returns 0, or -1 on allocation failure.
+ * max_entries > 0 stops after that many entries in visiting order (a bounded
+ * timing sample; later outputs are left untouched); <= 0 processes all.
  */
 int oracle_babai_naive(int64_t m, int64_t n, const double *W0, const double *LA,
                        const double *LB, const double *scale, int qmax,
                        const int8_t *forced, double tie_window, int8_t *codes,
-                       double *V, double *pre, int64_t *n_excused, int64_t *n_flip)
+                       double *V, double *pre, int64_t *n_excused, int64_t *n_flip,
+                       int64_t max_entries)
 {
     double *W = (double *)malloc(sizeof(double) * (size_t)(m * n));
     double *LAT = (double *)malloc(sizeof(double) * (size_t)(n * n));
@@ -76,11 +79,13 @@ int oracle_babai_naive(int64_t m, int64_t n, const double *W0, const double *LA,
     /* LAT[j*n + q] = LA[q*n + j]: column j of L^A stored contiguously */
     for (int64_t q = 0; q < n; ++q)
         for (int64_t j = 0; j < n; ++j) LAT[j * n + q] = LA[q * n + j];
-    int64_t exc = 0, flip = 0;
+    int64_t exc = 0, flip = 0, done = 0;
 
     for (int64_t i = 0; i < m; ++i) {
         const double s = scale[i];
         for (int64_t j = 0; j < n; ++j) {
+            if (max_entries > 0 && done >= max_entries) goto out;
+            ++done;
             const double w = W[i * n + j];
             int c;
             double x;
@@ -111,6 +116,7 @@ int oracle_babai_naive(int64_t m, int64_t n, const double *W0, const double *LA,
             }
         }
     }
+out:
     free(W);
     free(LAT);
     if (n_excused) *n_excused = exc;
@@ -127,13 +133,16 @@ int oracle_babai_naive(int64_t m, int64_t n, const double *W0, const double *LA,
  *   W~_pq = W0_pq - rhoB*E_{p-1,q} - rhoA*E_{p,q-1} + rhoA*rhoB*E_{p-1,q-1},
  *   E = V - W~.
  * O(mn) at any size; used as an exact reference for full-size structured runs.
+ * Tie forcing as for oracle_babai_naive.
  */
 int oracle_ar1_diffusion(int64_t m, int64_t n, const double *W0, double rhoA,
-                         double rhoB, const double *scale, int qmax, int8_t *codes,
-                         double *V, double *pre)
+                         double rhoB, const double *scale, int qmax, const int8_t *forced,
+                         double tie_window, int8_t *codes, double *V, double *pre,
+                         int64_t *n_excused, int64_t *n_flip)
 {
     double *E = (double *)malloc(sizeof(double) * (size_t)(m * n));
     if (!E) return -1;
+    int64_t exc = 0, flip = 0;
     for (int64_t p = 0; p < m; ++p) {
         const double s = scale[p];
         for (int64_t q = 0; q < n; ++q) {
@@ -144,7 +153,15 @@ int oracle_ar1_diffusion(int64_t m, int64_t n, const double *W0, double rhoA,
             int c;
             double x;
             if (s == 0.0) { c = 0; x = NAN; }
-            else { x = wt / s; c = quantise_code(x, qmax); }
+            else {
+                x = wt / s;
+                c = quantise_code(x, qmax);
+                if (forced && near_boundary(x, qmax, tie_window)) {
+                    ++exc;
+                    if ((int)forced[p * n + q] != c) ++flip;
+                    c = (int)forced[p * n + q];
+                }
+            }
             const double v = s * (double)c;
             codes[p * n + q] = (int8_t)c;
             V[p * n + q] = v;
@@ -153,5 +170,7 @@ int oracle_ar1_diffusion(int64_t m, int64_t n, const double *W0, double rhoA,
         }
     }
     free(E);
+    if (n_excused) *n_excused = exc;
+    if (n_flip) *n_flip = flip;
     return 0;
 }

@@ -61,11 +61,11 @@ def _load():
         lib.oracle_babai_naive.restype = ctypes.c_int
         lib.oracle_babai_naive.argtypes = [
             ctypes.c_int64, ctypes.c_int64, dp, dp, dp, dp, ctypes.c_int,
-            i8p, ctypes.c_double, i8p, dp, dp, i64p, i64p]
+            i8p, ctypes.c_double, i8p, dp, dp, i64p, i64p, ctypes.c_int64]
         lib.oracle_ar1_diffusion.restype = ctypes.c_int
         lib.oracle_ar1_diffusion.argtypes = [
             ctypes.c_int64, ctypes.c_int64, dp, ctypes.c_double, ctypes.c_double,
-            dp, ctypes.c_int, i8p, dp, dp]
+            dp, ctypes.c_int, i8p, ctypes.c_double, i8p, dp, dp, i64p, i64p]
         _lib = lib
     return _lib
 
@@ -109,9 +109,11 @@ def rev_cholesky(Xd) -> np.ndarray:
     return np.ascontiguousarray(C[::-1, ::-1].T)
 
 
-def babai(W, LA, LB, scale, bits: int, forced=None, tie_window: float = 0.0):
+def babai(W, LA, LB, scale, bits: int, forced=None, tie_window: float = 0.0,
+          max_entries: int = 0):
     """Sequential rounding of Alg. 2 (row-major), in C.  Returns a dict with
-    codes (int8), V (fp64), pre (x = W~/s, fp64), n_excused, n_flip."""
+    codes (int8), V (fp64), pre (x = W~/s, fp64), n_excused, n_flip.
+    max_entries > 0 stops after that many entries (timing samples only)."""
     lib = _load()
     W = np.ascontiguousarray(W, dtype=np.float64)
     m, n = W.shape
@@ -132,7 +134,7 @@ def babai(W, LA, LB, scale, bits: int, forced=None, tie_window: float = 0.0):
     rc = lib.oracle_babai_naive(m, n, _dptr(W), _dptr(LA), _dptr(LB), _dptr(s),
                                 qmax_of_bits(bits), fp, float(tie_window),
                                 _i8ptr(codes), _dptr(V), _dptr(pre),
-                                ctypes.byref(exc), ctypes.byref(flip))
+                                ctypes.byref(exc), ctypes.byref(flip), int(max_entries))
     if rc != 0:
         raise MemoryError("oracle_babai_naive: allocation failed")
     return dict(codes=codes, V=V, pre=pre, n_excused=int(exc.value),
@@ -149,7 +151,21 @@ def solve(W, A, B, damp_lambda: float, scale, bits: int, forced=None,
     return babai(W, LA, LB, scale, bits, forced=forced, tie_window=tie_window)
 
 
-def ar1_diffusion(W, rhoA: float, rhoB: float, scale, bits: int):
+def naive_macs(m: int, n: int, entries: int | None = None) -> float:
+    """Multiply-adds of Alg. 2's rank-one updates: entry (i, j) updates the
+    (m - i) x (n - j) block below-right of it; over the first `entries`
+    entries in row-major order (all if None)."""
+    if entries is None or entries >= m * n:
+        return m * (m + 1) / 2.0 * n * (n + 1) / 2.0
+    full_rows, rest = divmod(int(entries), n)
+    row_sum = n * (n + 1) / 2.0
+    total = sum((m - i) * row_sum for i in range(full_rows))
+    total += (m - full_rows) * sum(n - j for j in range(rest))
+    return float(total)
+
+
+def ar1_diffusion(W, rhoA: float, rhoB: float, scale, bits: int, forced=None,
+                  tie_window: float = 0.0):
     """Exact output for A = [rhoA^|i-j|], B = [rhoB^|i-j|] without damping."""
     lib = _load()
     W = np.ascontiguousarray(W, dtype=np.float64)
@@ -158,11 +174,19 @@ def ar1_diffusion(W, rhoA: float, rhoB: float, scale, bits: int):
     codes = np.zeros((m, n), np.int8)
     V = np.zeros((m, n), np.float64)
     pre = np.zeros((m, n), np.float64)
+    exc = ctypes.c_int64(0)
+    flip = ctypes.c_int64(0)
+    fp = None
+    if forced is not None:
+        forced = np.ascontiguousarray(forced, dtype=np.int8)
+        assert forced.shape == (m, n)
+        fp = _i8ptr(forced)
     rc = lib.oracle_ar1_diffusion(m, n, _dptr(W), float(rhoA), float(rhoB), _dptr(s),
-                                  qmax_of_bits(bits), _i8ptr(codes), _dptr(V), _dptr(pre))
+                                  qmax_of_bits(bits), fp, float(tie_window), _i8ptr(codes),
+                                  _dptr(V), _dptr(pre), ctypes.byref(exc), ctypes.byref(flip))
     if rc != 0:
         raise MemoryError("oracle_ar1_diffusion: allocation failed")
-    return dict(codes=codes, V=V, pre=pre)
+    return dict(codes=codes, V=V, pre=pre, n_excused=int(exc.value), n_flip=int(flip.value))
 
 
 def near_boundary(x, bits: int, window: float) -> np.ndarray:

@@ -1,0 +1,208 @@
+"""ctypes binding for libbakron.so -- argument marshalling only.
+
+Every step of the solver runs in the library's HIP kernels; torch is used only
+for device memory (``data_ptr()``) and the current HIP stream.  If the library
+has not been built, every call raises instead of falling back to anything.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libbakron.so")
+
+BAKRON_OK, BAKRON_EINVAL, BAKRON_ENOTSPD, BAKRON_ENOMEM, BAKRON_EHIP = range(5)
+
+EXPORTED = ("bakron_factor", "bakron_solve", "bakron_solve_debug", "bakron_factors_free",
+            "bakron_status_string", "bakron_factors_error", "bakron_last_error",
+            "bakron_factor_export", "bakron_profile_enable", "bakron_profile_read")
+
+_lib = None
+
+
+class BakronError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"{status_string(status) if _lib else status}: {msg}")
+        self.status = status
+
+
+class _Quantizer(ctypes.Structure):
+    _fields_ = [("bits", ctypes.c_int32), ("scale", ctypes.c_void_p)]
+
+
+class KernelStat(ctypes.Structure):
+    _fields_ = [("ms", ctypes.c_double), ("launches", ctypes.c_int64), ("flops", ctypes.c_double),
+                ("mfma_flops", ctypes.c_double)]
+
+    def as_dict(self):
+        return dict(ms=self.ms, launches=self.launches, flops=self.flops,
+                    mfma_flops=self.mfma_flops)
+
+
+def load(path: str = LIB_PATH):
+    """Load libbakron.so (raises if it is missing: there is no fallback)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is not built; run __graft_entry__.build() first")
+    lib = ctypes.CDLL(path)
+    vp = ctypes.c_void_p
+    lib.bakron_factor.restype = ctypes.c_int
+    lib.bakron_factor.argtypes = [vp, ctypes.c_int64, vp, ctypes.c_int64, ctypes.c_float, vp,
+                                  ctypes.POINTER(vp)]
+    lib.bakron_solve.restype = ctypes.c_int
+    lib.bakron_solve.argtypes = [vp, ctypes.c_int64, ctypes.c_int64, vp, _Quantizer, vp, vp, vp]
+    lib.bakron_solve_debug.restype = ctypes.c_int
+    lib.bakron_solve_debug.argtypes = [vp, ctypes.c_int64, ctypes.c_int64, vp, _Quantizer, vp, vp,
+                                       vp, vp]
+    lib.bakron_factors_free.restype = None
+    lib.bakron_factors_free.argtypes = [vp]
+    lib.bakron_status_string.restype = ctypes.c_char_p
+    lib.bakron_status_string.argtypes = [ctypes.c_int]
+    lib.bakron_factors_error.restype = ctypes.c_char_p
+    lib.bakron_factors_error.argtypes = [vp]
+    lib.bakron_last_error.restype = ctypes.c_char_p
+    lib.bakron_last_error.argtypes = []
+    lib.bakron_factor_export.restype = ctypes.c_int
+    lib.bakron_factor_export.argtypes = [vp, ctypes.c_int, vp, vp]
+    lib.bakron_profile_enable.restype = ctypes.c_int
+    lib.bakron_profile_enable.argtypes = [vp, ctypes.c_int]
+    lib.bakron_profile_read.restype = ctypes.c_int
+    lib.bakron_profile_read.argtypes = [vp, ctypes.POINTER(KernelStat), ctypes.POINTER(KernelStat),
+                                        ctypes.POINTER(KernelStat)]
+    _lib = lib
+    return lib
+
+
+def status_string(status: int) -> str:
+    return load().bakron_status_string(int(status)).decode()
+
+
+def _stream(torch, device):
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def _check_dev(t, name, dtype):
+    import torch
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise TypeError(f"{name} must be a CUDA (HIP) tensor")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+class Factors:
+    """Owns a bakron_factors handle (normalised L^A, L^B in fp32 on the device)."""
+
+    def __init__(self, handle: int, n: int, m: int | None, device):
+        self._h = ctypes.c_void_p(handle)
+        self.n = n
+        self.m = m
+        self.device = device
+
+    @property
+    def handle(self):
+        return self._h
+
+    def error(self) -> str:
+        return load().bakron_factors_error(self._h).decode()
+
+    def export(self, which: str):
+        """Dense fp32 copy of L^A ('A') or L^B ('B') for testing."""
+        import torch
+        d = self.n if which == "A" else (self.m or 0)
+        out = torch.empty((max(d, 1), max(d, 1)), dtype=torch.float32, device=self.device)
+        st = load().bakron_factor_export(self._h, 0 if which == "A" else 1,
+                                         ctypes.c_void_p(out.data_ptr()),
+                                         _stream(torch, self.device))
+        if st != BAKRON_OK:
+            raise BakronError(st, self.error())
+        return out
+
+    def profile(self, on: bool = True):
+        """Enable/disable per-launch event timing (measurement hook)."""
+        st = load().bakron_profile_enable(self._h, 1 if on else 0)
+        if st != BAKRON_OK:
+            raise BakronError(st, self.error())
+
+    def profile_read(self):
+        """Per-class stats of the last profiled solve (stream must be synchronised)."""
+        prep, leaf, node = KernelStat(), KernelStat(), KernelStat()
+        st = load().bakron_profile_read(self._h, ctypes.byref(prep), ctypes.byref(leaf),
+                                        ctypes.byref(node))
+        if st != BAKRON_OK:
+            raise BakronError(st, self.error())
+        return dict(prep=prep.as_dict(), leaf=leaf.as_dict(), node=node.as_dict())
+
+    def close(self):
+        if self._h is not None and self._h.value:
+            load().bakron_factors_free(self._h)
+            self._h = ctypes.c_void_p(0)
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def factor(A, B, damp: float) -> Factors:
+    """bakron_factor(A, B, damp) on the current stream.  B=None means I."""
+    import torch
+    lib = load()
+    _check_dev(A, "A", torch.float32)
+    n = A.shape[0]
+    if A.shape != (n, n):
+        raise ValueError("A must be square")
+    m = 0
+    bptr = None
+    if B is not None:
+        _check_dev(B, "B", torch.float32)
+        m = B.shape[0]
+        if B.shape != (m, m):
+            raise ValueError("B must be square")
+        bptr = ctypes.c_void_p(B.data_ptr())
+    h = ctypes.c_void_p(0)
+    st = lib.bakron_factor(ctypes.c_void_p(A.data_ptr()), n, bptr, m, float(damp),
+                           _stream(torch, A.device), ctypes.byref(h))
+    if st != BAKRON_OK:
+        raise BakronError(st, lib.bakron_last_error().decode())
+    return Factors(h.value, n, m if B is not None else None, A.device)
+
+
+def solve(W, f: Factors, bits: int, scale, codes=None, V=None, pre=None, debug: bool = False):
+    """bakron_solve / bakron_solve_debug on the current stream.
+
+    Returns (codes int8, V fp32) or (codes, V, pre) when debug=True.
+    """
+    import torch
+    lib = load()
+    _check_dev(W, "W", torch.float32)
+    _check_dev(scale, "scale", torch.float32)
+    m, n = W.shape
+    if scale.numel() != m:
+        raise ValueError("scale must have m entries")
+    if codes is None:
+        codes = torch.empty((m, n), dtype=torch.int8, device=W.device)
+    if V is None:
+        V = torch.empty((m, n), dtype=torch.float32, device=W.device)
+    _check_dev(codes, "codes", torch.int8)
+    _check_dev(V, "V", torch.float32)
+    q = _Quantizer(int(bits), ctypes.c_void_p(scale.data_ptr()).value)
+    s = _stream(torch, W.device)
+    if debug:
+        if pre is None:
+            pre = torch.empty((m, n), dtype=torch.float32, device=W.device)
+        _check_dev(pre, "pre", torch.float32)
+        st = lib.bakron_solve_debug(ctypes.c_void_p(W.data_ptr()), m, n, f.handle, q,
+                                    ctypes.c_void_p(codes.data_ptr()), ctypes.c_void_p(V.data_ptr()),
+                                    ctypes.c_void_p(pre.data_ptr()), s)
+    else:
+        st = lib.bakron_solve(ctypes.c_void_p(W.data_ptr()), m, n, f.handle, q,
+                              ctypes.c_void_p(codes.data_ptr()), ctypes.c_void_p(V.data_ptr()), s)
+    if st != BAKRON_OK:
+        raise BakronError(st, f.error())
+    return (codes, V, pre) if debug else (codes, V)

@@ -1,0 +1,364 @@
+// Factor kernels: damping and the normalised error-feedback factor of one
+// Kronecker factor X (n x n), computed in fp64 on the device.
+//
+//   X_d = X + damp * mean(diag X) * I                  (Sec. 4 opening; App. D)
+//   R   = RevCholesky(X_d): lower, positive diagonal, R^T R = X_d   (Sec. 3.1)
+//   L   = R^-1 diag(R): unit lower, equal to Cholesky(X_d^-1) with each column
+//         divided by its diagonal entry (Alg. 1 / Alg. 2, first two lines).
+//
+// RevCholesky is obtained from an ordinary Cholesky of the index-reversed
+// matrix: with P the reversal permutation, P X_d P = C C^T and R = P C^T P.
+// Hence R^-1 = P C^-T P and L[i][j] = Cinv[n-1-j][n-1-i] * C[n-1-j][n-1-j].
+//
+// Blocked right-looking Cholesky (block NB) and a recursive triangular
+// inverse, both driven by one fp64 tiled GEMM.  The result is rounded once to
+// fp32 and stored as packed lower-triangular TS x TS tiles for the solver.
+#include "common.h"
+
+namespace bk {
+
+constexpr int NB = 64;  // factor block
+
+// ---------------------------------------------------------------------------
+__global__ void k_diag_mean(const float* __restrict__ X, int64_t d, double* __restrict__ mean) {
+    __shared__ double part[256];
+    double s = 0.0;
+    for (int64_t i = threadIdx.x; i < d; i += blockDim.x) s += (double)X[i * d + i];
+    part[threadIdx.x] = s;
+    __syncthreads();
+    for (int w = 128; w > 0; w >>= 1) {
+        if ((int)threadIdx.x < w) part[threadIdx.x] += part[threadIdx.x + w];
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) *mean = part[0] / (double)d;
+}
+
+// Z[i][j] = X_d[d-1-i][d-1-j] (index-reversed, damped, fp64)
+__global__ void k_flip_damp(const float* __restrict__ X, int64_t d, const double* __restrict__ mean,
+                            double lam, double* __restrict__ Z) {
+    const int64_t total = d * d;
+    const double shift = lam * (*mean);
+    for (int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; idx < total;
+         idx += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t i = idx / d, j = idx - (idx / d) * d;
+        double v = (double)X[(d - 1 - i) * d + (d - 1 - j)];
+        if (i == j) v += shift;
+        Z[idx] = v;
+    }
+}
+
+// Unblocked Cholesky of the diagonal block Z[k0:k0+b, k0:k0+b] (lower part
+// only), one workgroup.  A non-positive or non-finite pivot sets *fail and
+// records the pivot index in the reversed ordering.
+__global__ __launch_bounds__(256) void k_potrf_diag(double* __restrict__ Z, int64_t ld, int64_t k0,
+                                                    int b, int* __restrict__ fail,
+                                                    int64_t* __restrict__ fail_pivot) {
+    if (*fail) return;
+    __shared__ double S[NB][NB + 1];
+    __shared__ double piv_s;
+    const int t = threadIdx.x;
+    for (int e = t; e < b * b; e += blockDim.x) {
+        const int i = e / b, j = e % b;
+        S[i][j] = (j <= i) ? Z[(k0 + i) * ld + (k0 + j)] : 0.0;
+    }
+    __syncthreads();
+    for (int j = 0; j < b; ++j) {
+        if (t == 0) piv_s = S[j][j];
+        __syncthreads();
+        const double piv = piv_s;
+        if (!(piv > 0.0) || !isfinite(piv)) {
+            if (t == 0) {
+                *fail = 1;
+                *fail_pivot = k0 + j;
+            }
+            return;  // uniform: every thread read the same pivot
+        }
+        const double dj = sqrt(piv);
+        __syncthreads();
+        for (int i = j + 1 + t; i < b; i += blockDim.x) S[i][j] /= dj;
+        if (t == 0) S[j][j] = dj;
+        __syncthreads();
+        const int r = b - j - 1;  // trailing order
+        for (int e = t; e < r * r; e += blockDim.x) {
+            const int i = j + 1 + e / r, c = j + 1 + e % r;
+            if (c <= i) S[i][c] -= S[i][j] * S[c][j];
+        }
+        __syncthreads();
+    }
+    for (int e = t; e < b * b; e += blockDim.x) {
+        const int i = e / b, j = e % b;
+        if (j <= i) Z[(k0 + i) * ld + (k0 + j)] = S[i][j];
+    }
+}
+
+// Inverse of lower-triangular diagonal blocks of C (size nbk <= NB each):
+// block g covers rows/cols [k0 + g*NB, min(d, k0 + g*NB + NB)) of C and is
+// written at rows/cols dst_off + g*NB of N (lower part only).  Thread j
+// computes column j by forward substitution.
+__global__ __launch_bounds__(NB) void k_inv_lower_blocks(const double* __restrict__ C, int64_t ldc,
+                                                         double* __restrict__ N, int64_t ldn,
+                                                         int64_t k0, int64_t d, int64_t dst_off,
+                                                         const int* __restrict__ fail) {
+    if (*fail) return;
+    __shared__ double S[NB][NB + 1];
+    __shared__ double Xs[NB][NB + 1];
+    const int64_t base = k0 + (int64_t)blockIdx.x * NB;
+    const int64_t dbase = dst_off + (int64_t)blockIdx.x * NB;
+    const int b = (int)((d - base) < NB ? (d - base) : NB);
+    const int t = threadIdx.x;
+    for (int i = 0; i < b; ++i)
+        if (t <= i) S[i][t] = C[(base + i) * ldc + (base + t)];
+    __syncthreads();
+    if (t < b) {
+        const int j = t;
+        for (int i = 0; i < b; ++i) {
+            double v;
+            if (i < j) v = 0.0;
+            else if (i == j) v = 1.0 / S[i][i];
+            else {
+                double acc = 0.0;
+                for (int k = j; k < i; ++k) acc += S[i][k] * Xs[k][j];
+                v = -acc / S[i][i];
+            }
+            Xs[i][j] = v;
+        }
+        for (int i = j; i < b; ++i) N[(dbase + i) * ldn + (dbase + j)] = Xs[i][j];
+    }
+}
+
+// C[M x N] = alpha * A[M x K] * op(B) + beta * C, row-major fp64.
+// op(B) = B (K x N, ldb) or B^T (B is N x K, ldb).  lower_only skips output
+// blocks lying entirely above the diagonal (row index < col index) of C.
+constexpr int GB = 64, GK = 16;
+__global__ __launch_bounds__(256) void k_gemm64(int64_t M, int64_t N, int64_t K, double alpha,
+                                                const double* __restrict__ A, int64_t lda,
+                                                const double* __restrict__ B, int64_t ldb,
+                                                int transB, double beta, double* __restrict__ C,
+                                                int64_t ldc, int lower_only,
+                                                const int* __restrict__ fail) {
+    if (*fail) return;
+    const int64_t r0 = (int64_t)blockIdx.y * GB, c0 = (int64_t)blockIdx.x * GB;
+    if (lower_only && c0 > r0 + GB - 1) return;
+    __shared__ double As[GK][GB + 1];
+    __shared__ double Bs[GK][GB + 1];
+    const int t = threadIdx.x;
+    const int tr = t / 16, tc = t % 16;
+    double acc[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = 0.0;
+    for (int64_t k0 = 0; k0 < K; k0 += GK) {
+        // A tile: GB rows x GK cols -> As[k][r]
+        for (int e = t; e < GB * GK; e += 256) {
+            const int r = e / GK, k = e % GK;
+            const int64_t gr = r0 + r, gk = k0 + k;
+            As[k][r] = (gr < M && gk < K) ? A[gr * lda + gk] : 0.0;
+        }
+        // op(B) tile: GK rows x GB cols -> Bs[k][c]
+        if (!transB) {
+            for (int e = t; e < GB * GK; e += 256) {
+                const int k = e / GB, c = e % GB;
+                const int64_t gk = k0 + k, gc = c0 + c;
+                Bs[k][c] = (gk < K && gc < N) ? B[gk * ldb + gc] : 0.0;
+            }
+        } else {
+            for (int e = t; e < GB * GK; e += 256) {
+                const int c = e / GK, k = e % GK;
+                const int64_t gk = k0 + k, gc = c0 + c;
+                Bs[k][c] = (gk < K && gc < N) ? B[gc * ldb + gk] : 0.0;
+            }
+        }
+        __syncthreads();
+#pragma unroll
+        for (int k = 0; k < GK; ++k) {
+            double a[4], bb[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) a[i] = As[k][tr * 4 + i];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) bb[j] = Bs[k][tc * 4 + j];
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int j = 0; j < 4; ++j) acc[i][j] = fma(a[i], bb[j], acc[i][j]);
+        }
+        __syncthreads();
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int64_t gr = r0 + tr * 4 + i;
+        if (gr >= M) continue;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int64_t gc = c0 + tc * 4 + j;
+            if (gc >= N) continue;
+            double* cp = C + gr * ldc + gc;
+            *cp = (beta == 0.0) ? alpha * acc[i][j] : alpha * acc[i][j] + beta * (*cp);
+        }
+    }
+}
+
+__global__ void k_copy2d(const double* __restrict__ src, int64_t lds, double* __restrict__ dst,
+                         int64_t ldd, int64_t rows, int64_t cols, const int* __restrict__ fail) {
+    if (*fail) return;
+    const int64_t total = rows * cols;
+    for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total;
+         e += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t r = e / cols, c = e - (e / cols) * cols;
+        dst[r * ldd + c] = src[r * lds + c];
+    }
+}
+
+// L[i][j] = Cinv[d-1-j][d-1-i] * C[d-1-j][d-1-j] for j <= i < d, rounded to
+// fp32 into packed TS x TS tiles; padding (index >= d) is the identity.
+__global__ void k_pack_factor(const double* __restrict__ C, const double* __restrict__ Ninv,
+                              int64_t d, int64_t ld, int64_t nt, float* __restrict__ out) {
+    const int64_t ntiles = nt * (nt + 1) / 2;
+    const int64_t total = ntiles * TILE_ELEMS;
+    for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total;
+         e += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t tile = e / TILE_ELEMS;
+        const int w = (int)(e - tile * TILE_ELEMS);
+        // invert tile = I(I+1)/2 + J
+        int64_t I = (int64_t)((sqrt(8.0 * (double)tile + 1.0) - 1.0) * 0.5);
+        while ((I + 1) * (I + 2) / 2 <= tile) ++I;
+        while (I * (I + 1) / 2 > tile) --I;
+        const int64_t J = tile - I * (I + 1) / 2;
+        const int64_t i = I * TS + w / TS, j = J * TS + w % TS;
+        float v;
+        if (i >= d || j >= d) v = (i == j) ? 1.0f : 0.0f;
+        else if (j > i) v = 0.0f;
+        else {
+            const int64_t a = d - 1 - j, c = d - 1 - i;
+            v = (float)(Ninv[a * ld + c] * C[a * ld + a]);
+        }
+        out[e] = v;
+    }
+}
+
+// Identity factor in packed storage (B = I: one-sided GPTQ, Sec. 1).
+__global__ void k_pack_identity(int64_t nt, float* __restrict__ out) {
+    const int64_t total = nt * (nt + 1) / 2 * TILE_ELEMS;
+    for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total;
+         e += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t tile = e / TILE_ELEMS;
+        const int w = (int)(e - tile * TILE_ELEMS);
+        int64_t I = (int64_t)((sqrt(8.0 * (double)tile + 1.0) - 1.0) * 0.5);
+        while ((I + 1) * (I + 2) / 2 <= tile) ++I;
+        while (I * (I + 1) / 2 > tile) --I;
+        const int64_t J = tile - I * (I + 1) / 2;
+        out[e] = (I == J && (w / TS) == (w % TS)) ? 1.0f : 0.0f;
+    }
+}
+
+// Dense row-major export of a packed factor (testing aid).
+__global__ void k_unpack_factor(const float* __restrict__ packed, int64_t d,
+                                float* __restrict__ dst) {
+    const int64_t total = d * d;
+    for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total;
+         e += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t i = e / d, j = e - (e / d) * d;
+        float v = 0.0f;
+        if (j <= i) v = packed[packed_tile_offset(i / TS, j / TS) + (i % TS) * TS + (j % TS)];
+        dst[e] = v;
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Host drivers
+
+static inline unsigned grid1d(int64_t total, int threads = 256) {
+    int64_t g = (total + threads - 1) / threads;
+    if (g > 65535LL * 64) g = 65535LL * 64;
+    if (g < 1) g = 1;
+    return (unsigned)g;
+}
+
+static hipError_t gemm64(hipStream_t s, int64_t M, int64_t N, int64_t K, double alpha,
+                         const double* A, int64_t lda, const double* B, int64_t ldb, int transB,
+                         double beta, double* C, int64_t ldc, int lower, const int* fail) {
+    if (M <= 0 || N <= 0) return hipSuccess;
+    dim3 grid((unsigned)((N + GB - 1) / GB), (unsigned)((M + GB - 1) / GB));
+    hipLaunchKernelGGL(k_gemm64, grid, dim3(256), 0, s, M, N, K, alpha, A, lda, B, ldb, transB,
+                       beta, C, ldc, lower, fail);
+    return hipGetLastError();
+}
+
+// Recursive lower-triangular inverse: Ninv[off:off+sz, off:off+sz] from C.
+// Diagonal NB-blocks must already be inverted.
+static hipError_t trtri_rec(hipStream_t s, const double* C, double* Ninv, int64_t ld, int64_t off,
+                            int64_t sz, double* T, const int* fail) {
+    if (sz <= NB) return hipSuccess;
+    int64_t nblk = (sz + NB - 1) / NB;
+    int64_t h = ((nblk + 1) / 2) * NB;
+    if (h >= sz) h = sz - NB;
+    hipError_t e = trtri_rec(s, C, Ninv, ld, off, h, T, fail);
+    if (e != hipSuccess) return e;
+    e = trtri_rec(s, C, Ninv, ld, off + h, sz - h, T, fail);
+    if (e != hipSuccess) return e;
+    const int64_t n2 = sz - h;
+    // T (n2 x h) = C21 * N11
+    e = gemm64(s, n2, h, h, 1.0, C + (off + h) * ld + off, ld, Ninv + off * ld + off, ld, 0, 0.0, T,
+               h, 0, fail);
+    if (e != hipSuccess) return e;
+    // N21 = -N22 * T
+    return gemm64(s, n2, h, n2, -1.0, Ninv + (off + h) * ld + (off + h), ld, T, h, 0, 0.0,
+                  Ninv + (off + h) * ld + off, ld, 0, fail);
+}
+
+// Factor one matrix.  Z, Ninv: d*d doubles; T: d*d/4 + d*NB doubles;
+// flag: 1 int + 1 int64 (fail, pivot) zeroed by the caller.
+hipError_t factor_one(hipStream_t s, const float* X, int64_t d, double lam, double* Z, double* Ninv,
+                      double* T, double* mean, int* fail, int64_t* fail_pivot, float* packed,
+                      int64_t nt) {
+    hipLaunchKernelGGL(k_diag_mean, dim3(1), dim3(256), 0, s, X, d, mean);
+    hipLaunchKernelGGL(k_flip_damp, dim3(grid1d(d * d)), dim3(256), 0, s, X, d, mean, lam, Z);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    for (int64_t k0 = 0; k0 < d; k0 += NB) {
+        const int b = (int)((d - k0) < NB ? (d - k0) : NB);
+        hipLaunchKernelGGL(k_potrf_diag, dim3(1), dim3(256), 0, s, Z, d, k0, b, fail, fail_pivot);
+        const int64_t rest = d - k0 - b;
+        if (rest > 0) {
+            // panel solve: P <- P * C_kk^-T via the explicit inverse of C_kk
+            double* Cinv = T;                 // NB x NB at the front of T
+            double* Ptmp = T + NB * NB;       // rest x b
+            hipMemsetAsync(Cinv, 0, sizeof(double) * NB * NB, s);
+            hipLaunchKernelGGL(k_inv_lower_blocks, dim3(1), dim3(NB), 0, s, Z, d, Cinv, (int64_t)NB,
+                               k0, k0 + b, (int64_t)0, fail);
+            e = gemm64(s, rest, b, b, 1.0, Z + (k0 + b) * d + k0, d, Cinv, NB, 1, 0.0, Ptmp, b, 0,
+                       fail);
+            if (e != hipSuccess) return e;
+            hipLaunchKernelGGL(k_copy2d, dim3(grid1d(rest * b)), dim3(256), 0, s, Ptmp, (int64_t)b,
+                               Z + (k0 + b) * d + k0, d, rest, (int64_t)b, fail);
+            // trailing update Z22 -= P P^T (lower blocks)
+            e = gemm64(s, rest, rest, b, -1.0, Z + (k0 + b) * d + k0, d, Z + (k0 + b) * d + k0, d, 1,
+                       1.0, Z + (k0 + b) * d + (k0 + b), d, 1, fail);
+            if (e != hipSuccess) return e;
+        }
+    }
+    // Ninv = C^-1 (lower); upper part must be zero for the recursive GEMMs
+    e = hipMemsetAsync(Ninv, 0, sizeof(double) * d * d, s);
+    if (e != hipSuccess) return e;
+    const int64_t nblk = (d + NB - 1) / NB;
+    hipLaunchKernelGGL(k_inv_lower_blocks, dim3((unsigned)nblk), dim3(NB), 0, s, Z, d, Ninv, d,
+                       (int64_t)0, d, (int64_t)0, fail);
+    e = trtri_rec(s, Z, Ninv, d, 0, d, T, fail);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k_pack_factor, dim3(grid1d(nt * (nt + 1) / 2 * TILE_ELEMS)), dim3(256), 0, s,
+                       Z, Ninv, d, d, nt, packed);
+    return hipGetLastError();
+}
+
+hipError_t pack_identity(hipStream_t s, int64_t nt, float* packed) {
+    hipLaunchKernelGGL(k_pack_identity, dim3(grid1d(nt * (nt + 1) / 2 * TILE_ELEMS)), dim3(256), 0,
+                       s, nt, packed);
+    return hipGetLastError();
+}
+
+hipError_t unpack_factor(hipStream_t s, const float* packed, int64_t d, float* dst) {
+    hipLaunchKernelGGL(k_unpack_factor, dim3(grid1d(d * d)), dim3(256), 0, s, packed, d, dst);
+    return hipGetLastError();
+}
+
+}  // namespace bk

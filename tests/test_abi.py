@@ -1,0 +1,73 @@
+"""C-ABI checks that need no GPU: the library loads, exports every entry point
+that include/bakron.h declares, and rejects invalid arguments on the host
+before touching the device."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "bakron.h")
+
+
+def _declared():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(bakron_[a-z_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    import paper_2608_06291_amd as pk
+    if not os.path.exists(pk.LIB_PATH):
+        pytest.fail("libbakron.so is not built (run __graft_entry__.build())")
+    return pk.load()
+
+
+def test_header_declares_the_boundary():
+    names = _declared()
+    for n in ("bakron_factor", "bakron_solve", "bakron_solve_debug", "bakron_factors_free",
+              "bakron_status_string"):
+        assert n in names
+
+
+def test_every_declared_symbol_is_exported(lib):
+    import paper_2608_06291_amd as pk
+    for name in _declared():
+        assert hasattr(lib, name), name
+    assert set(_declared()) == set(pk.EXPORTED)
+
+
+def test_status_strings(lib):
+    import paper_2608_06291_amd as pk
+    assert pk.status_string(0) == "BAKRON_OK"
+    assert pk.status_string(2) == "BAKRON_ENOTSPD"
+    assert pk.status_string(99) == "BAKRON_UNKNOWN"
+
+
+def test_host_validation_needs_no_device(lib):
+    """Null pointers / bad sizes / bad damping return EINVAL before any HIP call."""
+    import paper_2608_06291_amd as pk
+    h = ctypes.c_void_p(0)
+    st = lib.bakron_factor(None, 16, None, 0, 0.01, None, ctypes.byref(h))
+    assert st == pk.BAKRON_EINVAL and h.value is None
+    assert b"invalid" in lib.bakron_last_error()
+    st = lib.bakron_factor(ctypes.c_void_p(1), -3, None, 0, 0.01, None, ctypes.byref(h))
+    assert st == pk.BAKRON_EINVAL
+    st = lib.bakron_factor(ctypes.c_void_p(1), 16, None, 0, float("nan"), None, ctypes.byref(h))
+    assert st == pk.BAKRON_EINVAL
+    st = lib.bakron_factor(ctypes.c_void_p(1), 16, ctypes.c_void_p(1), 0, 0.01, None,
+                           ctypes.byref(h))
+    assert st == pk.BAKRON_EINVAL
+    q = pk._lib._Quantizer(4, 1)
+    assert lib.bakron_solve(ctypes.c_void_p(1), 4, 4, None, q, ctypes.c_void_p(1),
+                            ctypes.c_void_p(1), None) == pk.BAKRON_EINVAL
+    lib.bakron_factors_free(None)      # no-op
+
+
+def test_binding_refuses_cpu_tensors():
+    import torch
+    import paper_2608_06291_amd as pk
+    with pytest.raises(TypeError):
+        pk.factor(torch.eye(4), None, 0.01)

@@ -1,0 +1,93 @@
+"""GPU parity: the HIP solver (through the C ABI) against the fp64 oracle,
+element by element, on seeded inputs that span several 32x32 tiles with
+ragged tails, plus the degenerate shapes."""
+import numpy as np
+import pytest
+
+import workloads
+from gpu_util import check_against_oracle, gpu_run, log
+
+pytestmark = pytest.mark.gpu
+
+
+def _problem(m, n, seed, bits=4, identity_B=False):
+    return workloads.make_random(m, n, seed, bits=bits, identity_B=identity_B)
+
+
+SHAPES = [(1, 1), (1, 37), (37, 1), (2, 3), (31, 33), (32, 32), (33, 31), (64, 64),
+          (65, 97), (130, 67), (97, 200), (257, 129)]
+
+
+@pytest.mark.parametrize("m,n", SHAPES)
+def test_parity_shapes(oracle_mod, m, n):
+    p = _problem(m, n, seed=m * 1000 + n)
+    log(f"case shape m={m} n={n}")
+    codes, V, pre = gpu_run(p)
+    check_against_oracle(p, codes, V, pre, oracle_mod, label=f"shape{m}x{n}")
+
+
+@pytest.mark.parametrize("k", [0, 1, 3])
+@pytest.mark.parametrize("m,n", [(200, 300), (300, 200), (161, 161)])
+def test_parity_node_paths(oracle_mod, m, n, k):
+    """Small KNEAR sends most tile pairs through the divide-and-conquer nodes."""
+    p = _problem(m, n, seed=7 + m + n)
+    log(f"case node-path m={m} n={n} knear={k}")
+    codes, V, pre = gpu_run(p, k=k)
+    check_against_oracle(p, codes, V, pre, oracle_mod, label=f"knear{k}-{m}x{n}")
+
+
+@pytest.mark.parametrize("bits", [2, 3, 8])
+def test_parity_bits(oracle_mod, bits):
+    p = _problem(96, 130, seed=bits, bits=bits)
+    log(f"case bits={bits}")
+    codes, V, pre = gpu_run(p, k=2)
+    check_against_oracle(p, codes, V, pre, oracle_mod, label=f"bits{bits}")
+
+
+@pytest.mark.parametrize("m,n,k", [(65, 97, None), (200, 300, 1)])
+def test_parity_B_identity(oracle_mod, m, n, k):
+    """B = NULL: one-sided GPTQ with H = A (Sec. 1)."""
+    p = _problem(m, n, seed=3, identity_B=True)
+    log(f"case B=I m={m} n={n}")
+    codes, V, pre = gpu_run(p, k=k)
+    check_against_oracle(p, codes, V, pre, oracle_mod, label=f"BI-{m}x{n}")
+
+
+def test_zero_scale_rows(oracle_mod):
+    p = _problem(70, 90, seed=11)
+    p["scale"] = p["scale"].copy()
+    p["scale"][[0, 33, 69]] = 0.0
+    codes, V, pre = gpu_run(p, k=1)
+    assert np.all(codes[[0, 33, 69]] == 0) and np.all(V[[0, 33, 69]] == 0)
+    assert np.all(np.isnan(pre[[0, 33, 69]]))
+    check_against_oracle(p, codes, V, pre, oracle_mod, label="zero-scale")
+
+
+def test_config1_tiny_layer(oracle_mod):
+    """Configuration 1 (64x64, INT4) in full."""
+    p = workloads.make(1, seed=0)
+    codes, V, pre = gpu_run(p)
+    res = check_against_oracle(p, codes, V, pre, oracle_mod, label="config1")
+    assert res["margin"] < 1e-3
+
+
+def test_determinism(oracle_mod):
+    """Two solves give bitwise-identical codes, V and pre (no float atomics)."""
+    p = _problem(150, 170, seed=5)
+    (c1, v1, x1), (c2, v2, x2) = gpu_run(p, k=2, repeat=2)
+    assert np.array_equal(c1, c2)
+    assert np.array_equal(v1.view(np.uint32), v2.view(np.uint32))
+    assert np.array_equal(np.nan_to_num(x1).view(np.uint32), np.nan_to_num(x2).view(np.uint32))
+
+
+def test_ar1_structured_exact(oracle_mod):
+    """A, B AR(1) Toeplitz, no damping: exact O(mn) oracle (3-tap diffusion)."""
+    rng = np.random.default_rng(17)
+    m, n = 333, 290
+    W = (rng.standard_normal((m, n)) * 0.02).astype(np.float32)
+    p = dict(W=W, A=workloads.ar1_toeplitz(n, 0.5), B=workloads.ar1_toeplitz(m, 0.25),
+             scale=workloads.row_scales(W, 3), bits=3, damp=0.0)
+    codes, V, pre = gpu_run(p, k=2)
+    r = oracle_mod.ar1_diffusion(W, 0.5, 0.25, p["scale"], 3, forced=codes, tie_window=1e-4)
+    assert np.count_nonzero(r["codes"] != codes) == 0
+    assert r["n_flip"] <= 1e-4 * m * n
