@@ -7,6 +7,7 @@
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <algorithm>
 #include <new>
 #include <string>
 #include <vector>
@@ -21,7 +22,8 @@ hipError_t unpack_factor(hipStream_t s, const float* packed, int64_t d, float* d
 hipError_t run_schedule(hipStream_t s, const std::vector<SolveOp>& ops, const float* W, int64_t m,
                         int64_t n, int mt, int nt, float* X, float* Y, const float* LA,
                         const float* LB, int b_ident, const float* scale, float qmax,
-                        int8_t* codes, float* V, float* pre, int knear, hipEvent_t* evs);
+                        int8_t* codes, float* V, float* pre, int knear, const int4* items,
+                        hipEvent_t* evs);
 }  // namespace bk
 
 struct bakron_factors {
@@ -38,6 +40,8 @@ struct bakron_factors {
     float* Y = nullptr;
     int knear = 8;
     std::vector<bk::SolveOp> sched;
+    std::vector<int4> items_host;   // node work lists of the schedule
+    int4* items = nullptr;
     double prep_bytes = 0.0;
     // measurement hook
     int prof = 0;
@@ -78,13 +82,10 @@ static inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 static inline int imax(int a, int b) { return a > b ? a : b; }
 static inline int imin(int a, int b) { return a < b ? a : b; }
 
-// Algorithmic and MFMA-executed flops of one node launch, mirroring the
-// kernel's source ranges and masks.
-static void node_flops(const bk::SolveOp& op, int mt, int nt, int knear, int b_ident,
-                       double* flops, double* mfma) {
-    const double pair = 2.0 * bk::TS * bk::TS * bk::TS;
-    const double chunk = 2.0 * (bk::MACRO * bk::TS) * (bk::MACRO * bk::TS) * bk::TS;
-    double f = 0.0, x = 0.0;
+// Algorithmic flops of one node launch: 2*TS^3 per (source, target) tile
+// pair it pushes, mirroring the kernel's source ranges and masks.
+static double node_alg_flops(const bk::SolveOp& op, int mt, int nt, int knear, int b_ident) {
+    double f = 0.0;
     for (int D = op.Mid; D < op.L; ++D) {
         for (int I = imax(0, D - (nt - 1)); I <= imin(D, mt - 1); ++I) {
             const int J = D - I;
@@ -92,28 +93,47 @@ static void node_flops(const bk::SolveOp& op, int mt, int nt, int knear, int b_i
             f += imax(0, imin(op.Mid - I, J - knear) - imax(op.K - I, 0));
         }
     }
-    const int M = bk::MACRO, nmj = (nt + M - 1) / M;
-    for (int mi = 0; mi < op.gx; ++mi)
-        for (int md = op.md_lo; md < op.md_lo + op.gy; ++md) {
-            const int mj = md - mi;
-            if (mj < 0 || mj >= nmj) continue;
-            const int I0 = mi * M, J0 = mj * M;
-            if (I0 + J0 + 2 * (M - 1) < op.Mid || I0 + J0 >= op.L) continue;
+    return f * 2.0 * bk::TS * bk::TS * bk::TS;
+}
+
+// Work list of one node for MT x MT macro tiles: every (macro tile, push
+// kind) with at least one target tile in [Mid, L) and a non-empty source
+// range, longest source range first.
+static void node_items(int K, int Mid, int L, int mt, int nt, int knear, int b_ident, int MT,
+                       std::vector<int4>& out) {
+    out.clear();
+    const int nmi = (mt + MT - 1) / MT, nmj = (nt + MT - 1) / MT;
+    for (int mi = 0; mi < nmi; ++mi) {
+        const int I0 = mi * MT;
+        // macro columns whose tile anti-diagonals can meet [Mid, L)
+        const int mj_lo = imax(0, (Mid - 2 * (MT - 1) - I0 + MT - 1) / MT - 1);
+        for (int mj = mj_lo; mj < nmj; ++mj) {
+            const int J0 = mj * MT;
+            if (I0 + J0 >= L) break;
+            bool target = false;
+            for (int a = 0; a < MT && !target; ++a)
+                for (int b = 0; b < MT && !target; ++b) {
+                    const int I = I0 + a, J = J0 + b;
+                    target = I < mt && J < nt && I + J >= Mid && I + J < L;
+                }
+            if (!target) continue;
             if (!b_ident) {
-                const int lo = imax(0, op.K - (J0 + M - 1));
-                const int hi = imin(imin(op.Mid - J0, I0 + M - 1 - knear), mt);
-                if (hi > lo) x += (hi - lo) * chunk;
+                const int lo = imax(0, K - (J0 + MT - 1));
+                const int hi = imin(imin(Mid - J0, I0 + MT - 1 - knear), mt);
+                if (hi > lo) out.push_back(int4{I0, J0, (lo << 1) | 0, hi});
             }
-            const int lo = imax(0, op.K - (I0 + M - 1));
-            const int hi = imin(imin(op.Mid - I0, J0 + M - 1 - knear), nt);
-            if (hi > lo) x += (hi - lo) * chunk;
+            const int lo = imax(0, K - (I0 + MT - 1));
+            const int hi = imin(imin(Mid - I0, J0 + MT - 1 - knear), nt);
+            if (hi > lo) out.push_back(int4{I0, J0, (lo << 1) | 1, hi});
         }
-    *flops = f * pair;
-    *mfma = x;
+    }
+    std::stable_sort(out.begin(), out.end(), [](const int4& u, const int4& v) {
+        return (u.w - (u.z >> 1)) > (v.w - (v.z >> 1));
+    });
 }
 
 static void build_schedule(int K, int L, int mt, int nt, int knear, int b_ident,
-                           std::vector<bk::SolveOp>& ops) {
+                           std::vector<bk::SolveOp>& ops, std::vector<int4>& items) {
     if (L - K == 1) {
         bk::SolveOp op{};
         op.kind = 0;
@@ -138,25 +158,33 @@ static void build_schedule(int K, int L, int mt, int nt, int knear, int b_ident,
         return;
     }
     const int Mid = (K + L) / 2;
-    build_schedule(K, Mid, mt, nt, knear, b_ident, ops);
+    build_schedule(K, Mid, mt, nt, knear, b_ident, ops, items);
     if (L - K > knear + 1) {
         bk::SolveOp op{};
         op.kind = 1;
         op.K = K;
         op.Mid = Mid;
         op.L = L;
-        const int M = bk::MACRO;  // macro tile edge in solver tiles
-        int lo = Mid - 2 * (M - 1);
-        op.md_lo = lo <= 0 ? 0 : (int)cdiv(lo, M);
-        const int md_hi = (L - 1) / M;
-        op.gx = (int)cdiv(mt, M);
-        op.gy = md_hi - op.md_lo + 1;
-        if (op.gy > 0) {
-            node_flops(op, mt, nt, knear, b_ident, &op.flops, &op.mfma_flops);
+        std::vector<int4> its;
+        // 128 x 128 workgroups when they fill the chip twice over, else 64 x 64
+        op.macro = bk::MACRO;
+        node_items(K, Mid, L, mt, nt, knear, b_ident, 4, its);
+        if ((int)its.size() < 512) {
+            op.macro = 2;
+            node_items(K, Mid, L, mt, nt, knear, b_ident, 2, its);
+        }
+        if (!its.empty()) {
+            op.item_off = (int)items.size();
+            op.item_cnt = (int)its.size();
+            const double chunk = 2.0 * (op.macro * bk::TS) * (op.macro * bk::TS) * bk::TS;
+            op.mfma_flops = 0.0;
+            for (const int4& it : its) op.mfma_flops += (it.w - (it.z >> 1)) * chunk;
+            op.flops = node_alg_flops(op, mt, nt, knear, b_ident);
+            items.insert(items.end(), its.begin(), its.end());
             ops.push_back(op);
         }
     }
-    build_schedule(Mid, L, mt, nt, knear, b_ident, ops);
+    build_schedule(Mid, L, mt, nt, knear, b_ident, ops, items);
 }
 
 extern "C" bakron_status bakron_factor(const float* A, int64_t n, const float* B, int64_t m,
@@ -265,6 +293,7 @@ extern "C" void bakron_factors_free(bakron_factors* f) {
     if (f->LB) hipFree(f->LB);
     if (f->X) hipFree(f->X);
     if (f->Y) hipFree(f->Y);
+    if (f->items) hipFree(f->items);
     for (hipEvent_t ev : f->evs) hipEventDestroy(ev);
     if (cur != f->device) hipSetDevice(cur);
     delete f;
@@ -291,7 +320,16 @@ static bakron_status ensure_workspace(bakron_factors* f, int64_t m, int64_t n) {
         f->LB_tiles = mt;
     }
     f->sched.clear();
-    build_schedule(0, (int)(mt + nt - 1), (int)mt, (int)nt, f->knear, f->b_ident, f->sched);
+    f->items_host.clear();
+    build_schedule(0, (int)(mt + nt - 1), (int)mt, (int)nt, f->knear, f->b_ident, f->sched,
+                   f->items_host);
+    if (f->items) { hipFree(f->items); f->items = nullptr; }
+    if (!f->items_host.empty()) {
+        const size_t ib = sizeof(int4) * f->items_host.size();
+        e = hipMalloc(&f->items, ib);
+        if (e == hipSuccess) e = hipMemcpy(f->items, f->items_host.data(), ib, hipMemcpyHostToDevice);
+        if (e != hipSuccess) return hip_fail(&f->err, e, "bakron_solve: work list upload");
+    }
     f->prep_bytes = (double)m * n * 4.0 + 2.0 * 4.0 * mt * nt * bk::TILE_ELEMS;
     f->ws_m = m;
     f->ws_n = n;
@@ -337,7 +375,8 @@ static bakron_status solve_impl(const float* W, int64_t m, int64_t n, const bakr
         evs = f->evs.data();
     }
     hipError_t e = bk::run_schedule(stream, f->sched, W, m, n, mt, nt, f->X, f->Y, f->LA, f->LB,
-                                    f->b_ident, q.scale, qmax, codes, V, pre, f->knear, evs);
+                                    f->b_ident, q.scale, qmax, codes, V, pre, f->knear, f->items,
+                                    evs);
     if (e != hipSuccess) return hip_fail(&f->err, e, "bakron_solve: launch");
     f->prof_valid = f->prof;
     return BAKRON_OK;

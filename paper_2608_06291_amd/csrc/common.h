@@ -37,9 +37,15 @@ __host__ __device__ inline int64_t ws_tile_offset(int64_t I, int64_t J, int64_t 
 struct SolveOp {
     int kind;          // 0 = leaf, 1 = node
     int D, I_lo, ntiles;
-    int K, Mid, L, md_lo, gx, gy;
+    int K, Mid, L;
+    int macro;         // node: solver tiles per workgroup edge (4 or 2)
+    int item_off, item_cnt;  // node: slice of the work list
     double flops;
     double mfma_flops;
 };
+
+// Node work-list item (int4): x = first tile row I0, y = first tile column
+// J0 of the MT x MT macro tile, z = (first source tile << 1) | push kind
+// (0 column push, 1 row push), w = end of the source tile range.
 
 }  // namespace bk

@@ -63,11 +63,12 @@ struct LeafArgs {
 // The coefficients are held in registers, each thread's factor row rotated so
 // that step d reads register (d mod 32): no dynamic register indexing.
 __global__ __launch_bounds__(1024) void k_leaf(LeafArgs a) {
-    __shared__ float LBt[TS][TS + 1];
-    __shared__ float LAt[TS][TS + 1];
+    __shared__ float LBt[TS][TS];            // unpadded: the rotated reads below are conflict-free
+    __shared__ float LAt[TS][TS];
     __shared__ float Et[TS][TS + 1];
     __shared__ float Ft[TS][TS + 1];
-    __shared__ float Pw[16][TS][TS + 1];   // per-wave factor tile for pushes
+    __shared__ float Pw[16][TS][TS + 1];     // per-wave push factor tile (prefetched)
+    __shared__ float Ow[16][TILE_ELEMS];     // per-wave push target tile, fragment order (prefetched)
     __shared__ float Ecol[2][TS];
     __shared__ float Frow[2][TS];
 
@@ -78,15 +79,57 @@ __global__ __launch_bounds__(1024) void k_leaf(LeafArgs a) {
     const int c = 2 * w + (l >> 5);
     const int p = l & 31;
     const int q = (c - p) & 31;
+    const int lr = l & 31, lk = l >> 5;
+
+    // Near push of this wave: target kk = w/2 + 1 tiles below (even w, column
+    // push into Y) or to the right (odd w, row push into X).  The factor tile
+    // and the target tile do not change during this launch, so both are
+    // fetched now and the push at the end touches no global memory before its
+    // final store.
+    const int kk = (w >> 1) + 1;
+    const bool colpush = (w & 1) == 0;
+    int TI = I, TJ = J;
+    bool active = kk <= a.knear;
+    const float* fac = nullptr;
+    if (colpush) {
+        TI = I + kk;
+        active = active && !a.b_ident && TI < a.mt;
+        if (active) fac = a.LB + packed_tile_offset(TI, I);
+    } else {
+        TJ = J + kk;
+        active = active && TJ < a.nt;
+        if (active) fac = a.LA + packed_tile_offset(TJ, J);
+    }
+    float* out = colpush ? a.Y : a.X;
+    const int64_t to = ws_tile_offset(TI, TJ, a.nt);
+    if (active) {
+#pragma unroll
+        for (int s4 = 0; s4 < 4; ++s4) {
+            const int e0 = (s4 * 64 + l) * 4;
+            const f32x4 v = *reinterpret_cast<const f32x4*>(fac + e0);
+            const int r = e0 >> 5, cc = e0 & 31;
+            Pw[w][r][cc] = v[0];
+            Pw[w][r][cc + 1] = v[1];
+            Pw[w][r][cc + 2] = v[2];
+            Pw[w][r][cc + 3] = v[3];
+        }
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            const int rr = (r >> 2) * 8 + lk * 4 + (r & 3);
+            Ow[w][r * 64 + l] = out[to + rr * TS + lr];
+        }
+    }
 
     {   // diagonal factor tiles
         const int r = tid >> 5, cc = tid & 31;
         LAt[r][cc] = a.LA[packed_tile_offset(J, J) + tid];
         LBt[r][cc] = a.b_ident ? (r == cc ? 1.0f : 0.0f) : a.LB[packed_tile_offset(I, I) + tid];
     }
-    const int64_t xo = ws_tile_offset(I, J, a.nt) + p * TS + q;
+    const int64_t tbase = ws_tile_offset(I, J, a.nt);
+    const int64_t xo = tbase + q * TS + p;     // X tiles are column-major
+    const int64_t yo = tbase + p * TS + q;     // Y tiles are row-major
     float h = a.X[xo];
-    float g = a.Y[xo];
+    float g = a.Y[yo];
     const int64_t row = (int64_t)I * TS + p, col = (int64_t)J * TS + q;
     const float s = (row < a.m) ? a.scale[row] : 0.0f;
     const float inv_s = (s > 0.0f) ? 1.0f / s : 0.0f;
@@ -141,7 +184,7 @@ __global__ __launch_bounds__(1024) void k_leaf(LeafArgs a) {
     }
 
     a.X[xo] = e_out;
-    a.Y[xo] = f_out;
+    a.Y[yo] = f_out;
     if (row < a.m && col < a.n) {
         const int64_t o = row * a.n + col;
         a.codes[o] = (int8_t)c_out;
@@ -152,57 +195,24 @@ __global__ __launch_bounds__(1024) void k_leaf(LeafArgs a) {
     Ft[p][q] = f_out;
     __syncthreads();
 
-    // Near pushes: wave w handles target k = w/2 + 1, column push (even w)
-    // or row push (odd w), one 32x32x32 product on fp32 MFMA.
-    const int kk = (w >> 1) + 1;
-    const bool colpush = (w & 1) == 0;
-    bool active = kk <= a.knear;
-    int TI = I, TJ = J;
-    const float* fac = nullptr;
-    if (colpush) {
-        TI = I + kk;
-        active = active && !a.b_ident && TI < a.mt;
-        if (active) fac = a.LB + packed_tile_offset(TI, I);
-    } else {
-        TJ = J + kk;
-        active = active && TJ < a.nt;
-        if (active) fac = a.LA + packed_tile_offset(TJ, J);
-    }
     if (!active) return;   // wave-uniform; no barrier follows
-#pragma unroll
-    for (int s4 = 0; s4 < 4; ++s4) {
-        const int e0 = (s4 * 64 + l) * 4;
-        const f32x4 v = *reinterpret_cast<const f32x4*>(fac + e0);
-        const int r = e0 >> 5, cc = e0 & 31;
-        Pw[w][r][cc] = v[0];
-        Pw[w][r][cc + 1] = v[1];
-        Pw[w][r][cc + 2] = v[2];
-        Pw[w][r][cc + 3] = v[3];
-    }
-    // intra-wave handoff of the LDS tile (other lanes' writes)
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     f32x16 acc = {0};
-    const int lr = l & 31, lk = l >> 5;
 #pragma unroll
     for (int k0 = 0; k0 < TS; k0 += 2) {
         float av, bv;
-        if (colpush) {            // L^B[TI, I] (32x32) * E (32x32)
+        if (colpush) {            // Y[TI, J] += L^B[TI, I] (32x32) * E (32x32)
             av = Pw[w][lr][k0 + lk];
             bv = Et[k0 + lk][lr];
-        } else {                  // F (32x32) * (L^A[TJ, J])^T
-            av = Ft[lr][k0 + lk];
-            bv = Pw[w][lr][k0 + lk];
+        } else {                  // X[I, TJ]^T += L^A[TJ, J] * F^T (X is column-major)
+            av = Pw[w][lr][k0 + lk];
+            bv = Ft[lr][k0 + lk];
         }
         acc = __builtin_amdgcn_mfma_f32_32x32x2f32(av, bv, acc, 0, 0, 0);
     }
-    float* out = colpush ? a.Y : a.X;
-    const int64_t to = ws_tile_offset(TI, TJ, a.nt);
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
         const int rr = (r >> 2) * 8 + lk * 4 + (r & 3);
-        out[to + rr * TS + lr] += acc[r];
+        out[to + rr * TS + lr] = Ow[w][r * 64 + l] + acc[r];
     }
 }
 
@@ -210,143 +220,172 @@ struct NodeArgs {
     int K, Mid, L;    // tile anti-diagonal range [K, L), split at Mid
     int knear;
     int mt, nt;
-    int md_lo;        // first macro anti-diagonal of the grid
     float* X;
     float* Y;
     const float* LA;
     const float* LB;
-    int b_ident;      // B = I: column pushes vanish
+    const int4* items;  // work list of this launch (see NodeItem in common.h)
 };
 
 // Band push of one divide-and-conquer node on fp32 MFMA.
-// Workgroup = 128x128 output macro tile (4x4 solver tiles), 4 waves of 64x64
-// (2x2 blocks of v_mfma_f32_32x32x2f32).  blockIdx.z = 0: column push into Y;
-// 1: row push into X.  The (source, target) validity masks are separable, so
-// each K step stages zero tiles for invalid sources and the products of the
-// remaining tiles are exact.
-__global__ __launch_bounds__(256) void k_node(NodeArgs a) {
-    __shared__ float As[MACRO * TS][TS + 1];
-    __shared__ float Bs[TS][MACRO * TS + 1];
-    const int mi = blockIdx.x;
-    const int md = a.md_lo + (int)blockIdx.y;
-    const int mj = md - mi;
-    const int nmj = (a.nt + MACRO - 1) / MACRO;
-    if (mj < 0 || mj >= nmj) return;
-    const int I0 = mi * MACRO, J0 = mj * MACRO;
-    if (I0 + J0 + 2 * (MACRO - 1) < a.Mid || I0 + J0 >= a.L) return;
-    const bool colpush = blockIdx.z == 0;
-    if (colpush && a.b_ident) return;
-    int klo, khi;
-    if (colpush) {
-        klo = max(0, a.K - (J0 + MACRO - 1));
-        khi = min(min(a.Mid - J0, I0 + MACRO - 1 - a.knear), a.mt);
-    } else {
-        klo = max(0, a.K - (I0 + MACRO - 1));
-        khi = min(min(a.Mid - I0, J0 + MACRO - 1 - a.knear), a.nt);
-    }
-    if (klo >= khi) return;
+//
+// Both pushes are computed as C[M][N] += sum_k A[M][k] * B[N][k] over source
+// tiles kt (K chunks of TS), with every operand tile stored [row][k]:
+//   column push: C = Y[I, J] (row-major), A = L^B[I, kt], B = E[kt, J] read
+//                from X, whose tiles are column-major (= E^T);
+//   row push:    C = X[I, J] stored column-major, i.e. C^T[J][I]
+//                = sum L^A[J, kt] * F[I, kt]^T, A = L^A[J, kt], B = F[I, kt]
+//                read from Y (row-major).
+// So every global -> LDS copy is a straight 16-byte copy and every output
+// write is coalesced.  A workgroup computes MT x MT solver tiles with 4 waves
+// in a 2 x 2 arrangement (each wave MT/2 x MT/2 blocks of
+// v_mfma_f32_32x32x2f32).  Inside a K chunk the 32 k's are split between the
+// two lane halves (half h takes k = 16h + s at step s), so each lane reads 16
+// consecutive floats per operand with four 16-byte LDS loads.  LDS is double
+// buffered and the next chunk is prefetched into registers while the current
+// one is multiplied.  The (source, target) validity masks are separable, so
+// invalid source tiles are staged as zeros and the sums stay exact.
+//
+// One workgroup per work-list item: the host lists only items with a
+// non-empty source range, longest first, so the long K loops start early.
+constexpr int LDS_STRIDE = TS + 4;   // 36 floats: 16-byte rows, no b128 bank conflicts
+template <int MT>
+__global__ __launch_bounds__(256, (MT == 4 ? 2 : 4)) void k_node(NodeArgs a) {
+    constexpr int WB = MT / 2;       // 32x32 blocks per wave per dimension
+    __shared__ __attribute__((aligned(16))) float As[2][MT * TS][LDS_STRIDE];
+    __shared__ __attribute__((aligned(16))) float Bs[2][MT * TS][LDS_STRIDE];
+    const int4 it = a.items[blockIdx.x];
+    const int I0 = it.x, J0 = it.y;
+    const bool colpush = (it.z & 1) == 0;
+    const int klo = it.z >> 1, khi = it.w;
 
     const int tid = threadIdx.x;
     const int wv = tid >> 6, l = tid & 63;
     const int wm = wv >> 1, wn = wv & 1;
     const int lr = l & 31, lk = l >> 5;
-    f32x16 acc[2][2];
-#pragma unroll
-    for (int x = 0; x < 2; ++x)
-#pragma unroll
-        for (int y = 0; y < 2; ++y) acc[x][y] = f32x16{0};
+    const int srow = tid >> 3, sk = (tid & 7) * 4;   // staging: one float4 of each tile
 
+    auto a_tile = [&](int t, int kt) -> const float* {
+        if (colpush) {
+            const int I = I0 + t;
+            return (I < a.mt && kt <= I - a.knear - 1) ? a.LB + packed_tile_offset(I, kt) : nullptr;
+        }
+        const int J = J0 + t;
+        return (J < a.nt && kt <= J - a.knear - 1) ? a.LA + packed_tile_offset(J, kt) : nullptr;
+    };
+    auto b_tile = [&](int t, int kt) -> const float* {
+        if (colpush) {
+            const int J = J0 + t;
+            return (J < a.nt && kt + J >= a.K && kt + J < a.Mid) ? a.X + ws_tile_offset(kt, J, a.nt)
+                                                                 : nullptr;
+        }
+        const int I = I0 + t;
+        return (I < a.mt && I + kt >= a.K && I + kt < a.Mid) ? a.Y + ws_tile_offset(I, kt, a.nt)
+                                                             : nullptr;
+    };
+    f32x4 ra[MT], rb[MT];
+    auto load = [&](int kt) {
+#pragma unroll
+        for (int t = 0; t < MT; ++t) {
+            const float* pa = a_tile(t, kt);
+            const float* pb = b_tile(t, kt);
+            ra[t] = pa ? *reinterpret_cast<const f32x4*>(pa + tid * 4) : f32x4{0.f, 0.f, 0.f, 0.f};
+            rb[t] = pb ? *reinterpret_cast<const f32x4*>(pb + tid * 4) : f32x4{0.f, 0.f, 0.f, 0.f};
+        }
+    };
+    auto store = [&](int s) {
+#pragma unroll
+        for (int t = 0; t < MT; ++t) {
+            *reinterpret_cast<f32x4*>(&As[s][t * TS + srow][sk]) = ra[t];
+            *reinterpret_cast<f32x4*>(&Bs[s][t * TS + srow][sk]) = rb[t];
+        }
+    };
+
+    f32x16 acc[WB][WB];
+#pragma unroll
+    for (int x = 0; x < WB; ++x)
+#pragma unroll
+        for (int y = 0; y < WB; ++y) acc[x][y] = f32x16{0};
+
+    load(klo);
+    store(0);
+    __syncthreads();
     for (int kt = klo; kt < khi; ++kt) {
-        // stage A (128 x 32) and B (32 x 128): tile t = 0..3 of each
+        const int s = (kt - klo) & 1;
+        const bool more = kt + 1 < khi;
+        if (more) load(kt + 1);
+        f32x4 fa[WB][4], fb[WB][4];
 #pragma unroll
-        for (int t = 0; t < MACRO; ++t) {
-            const int e0 = tid * 4;              // 256 threads x 4 = one tile
-            const int r = e0 >> 5, cc = e0 & 31;
-            // A operand
-            const float* src = nullptr;
-            if (colpush) {
-                const int I = I0 + t;
-                if (I < a.mt && kt <= I - a.knear - 1) src = a.LB + packed_tile_offset(I, kt);
-            } else {
-                const int I = I0 + t;
-                if (I < a.mt && I + kt >= a.K && I + kt < a.Mid)
-                    src = a.Y + ws_tile_offset(I, kt, a.nt);
-            }
-            f32x4 v = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-            if (src) v = *reinterpret_cast<const f32x4*>(src + e0);
-            As[t * TS + r][cc] = v[0];
-            As[t * TS + r][cc + 1] = v[1];
-            As[t * TS + r][cc + 2] = v[2];
-            As[t * TS + r][cc + 3] = v[3];
-            // B operand
-            const float* bsrc = nullptr;
-            if (colpush) {
-                const int J = J0 + t;
-                if (J < a.nt && kt + J >= a.K && kt + J < a.Mid)
-                    bsrc = a.X + ws_tile_offset(kt, J, a.nt);
-            } else {
-                const int J = J0 + t;
-                if (J < a.nt && kt <= J - a.knear - 1) bsrc = a.LA + packed_tile_offset(J, kt);
-            }
-            f32x4 u = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-            if (bsrc) u = *reinterpret_cast<const f32x4*>(bsrc + e0);
-            if (colpush) {       // E tile rows are the K index
-                Bs[r][t * TS + cc] = u[0];
-                Bs[r][t * TS + cc + 1] = u[1];
-                Bs[r][t * TS + cc + 2] = u[2];
-                Bs[r][t * TS + cc + 3] = u[3];
-            } else {             // L^A tile (J, kt): element [jr][jc] -> Bs[jc][t*TS + jr]
-                Bs[cc][t * TS + r] = u[0];
-                Bs[cc + 1][t * TS + r] = u[1];
-                Bs[cc + 2][t * TS + r] = u[2];
-                Bs[cc + 3][t * TS + r] = u[3];
-            }
+        for (int x = 0; x < WB; ++x)
+#pragma unroll
+            for (int v = 0; v < 4; ++v)
+                fa[x][v] = *reinterpret_cast<const f32x4*>(
+                    &As[s][(wm * WB + x) * TS + lr][lk * 16 + v * 4]);
+#pragma unroll
+        for (int y = 0; y < WB; ++y)
+#pragma unroll
+            for (int v = 0; v < 4; ++v)
+                fb[y][v] = *reinterpret_cast<const f32x4*>(
+                    &Bs[s][(wn * WB + y) * TS + lr][lk * 16 + v * 4]);
+#pragma unroll
+        for (int st = 0; st < 16; ++st) {
+#pragma unroll
+            for (int x = 0; x < WB; ++x)
+#pragma unroll
+                for (int y = 0; y < WB; ++y)
+                    acc[x][y] = __builtin_amdgcn_mfma_f32_32x32x2f32(fa[x][st >> 2][st & 3],
+                                                                    fb[y][st >> 2][st & 3],
+                                                                    acc[x][y], 0, 0, 0);
         }
-        __syncthreads();
-#pragma unroll
-        for (int k0 = 0; k0 < TS; k0 += 2) {
-            float av[2], bv[2];
-#pragma unroll
-            for (int x = 0; x < 2; ++x) av[x] = As[wm * 64 + x * 32 + lr][k0 + lk];
-#pragma unroll
-            for (int y = 0; y < 2; ++y) bv[y] = Bs[k0 + lk][wn * 64 + y * 32 + lr];
-#pragma unroll
-            for (int x = 0; x < 2; ++x)
-#pragma unroll
-                for (int y = 0; y < 2; ++y)
-                    acc[x][y] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[x], bv[y], acc[x][y], 0, 0, 0);
-        }
+        if (more) store(s ^ 1);
         __syncthreads();
     }
 
-    float* out = colpush ? a.Y : a.X;
+    // epilogue: block (x, y) of wave (wm, wn) is output solver tile
+    // (M tile wm*WB+x, N tile wn*WB+y); C[M][N] row-major inside the tile.
 #pragma unroll
-    for (int x = 0; x < 2; ++x)
+    for (int x = 0; x < WB; ++x)
 #pragma unroll
-        for (int y = 0; y < 2; ++y) {
-            const int I = I0 + wm * 2 + x, J = J0 + wn * 2 + y;
+        for (int y = 0; y < WB; ++y) {
+            const int tm = wm * WB + x, tn = wn * WB + y;
+            const int I = colpush ? I0 + tm : I0 + tn;
+            const int J = colpush ? J0 + tn : J0 + tm;
             if (I >= a.mt || J >= a.nt || I + J < a.Mid || I + J >= a.L) continue;
-            const int64_t to = ws_tile_offset(I, J, a.nt);
+            float* out = (colpush ? a.Y : a.X) + ws_tile_offset(I, J, a.nt);
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
                 const int rr = (r >> 2) * 8 + lk * 4 + (r & 3);
-                out[to + rr * TS + lr] += acc[x][y][r];
+                out[rr * TS + lr] += acc[x][y][r];
             }
         }
 }
 
-// X <- W (tile-major, zero padding), Y <- 0.
-__global__ void k_prep(const float* __restrict__ W, int64_t m, int64_t n, int mt, int nt,
-                       float* __restrict__ X, float* __restrict__ Y) {
-    const int64_t total = (int64_t)mt * nt * TILE_ELEMS;
-    for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total;
-         e += (int64_t)gridDim.x * blockDim.x) {
-        const int64_t tile = e / TILE_ELEMS;
-        const int w = (int)(e - tile * TILE_ELEMS);
-        const int64_t I = tile / nt, J = tile - (tile / nt) * nt;
-        const int64_t r = I * TS + w / TS, cc = J * TS + w % TS;
-        X[e] = (r < m && cc < n) ? W[r * n + cc] : 0.0f;
-        Y[e] = 0.0f;
+// X <- W (tile-major, column-major inside each tile, zero padding), Y <- 0.
+// One workgroup per tile; the transpose goes through LDS so that both the
+// read of W and the write of X are coalesced.
+__global__ __launch_bounds__(256) void k_prep(const float* __restrict__ W, int64_t m, int64_t n,
+                                              int mt, int nt, float* __restrict__ X,
+                                              float* __restrict__ Y) {
+    __shared__ float T[TS][TS + 1];
+    const int64_t tile = blockIdx.x;
+    const int64_t I = tile / nt, J = tile - (tile / nt) * nt;
+    const int tid = threadIdx.x;
+#pragma unroll
+    for (int k = 0; k < TILE_ELEMS / 256; ++k) {
+        const int e = k * 256 + tid;
+        const int r = e >> 5, c = e & 31;
+        const int64_t gr = I * TS + r, gc = J * TS + c;
+        T[r][c] = (gr < m && gc < n) ? W[gr * n + gc] : 0.0f;
+    }
+    __syncthreads();
+    float* x = X + tile * TILE_ELEMS;
+    float* y = Y + tile * TILE_ELEMS;
+#pragma unroll
+    for (int k = 0; k < TILE_ELEMS / 256; ++k) {
+        const int e = k * 256 + tid;
+        const int c = e >> 5, r = e & 31;
+        x[e] = T[r][c];
+        y[e] = 0.0f;
     }
 }
 
@@ -355,10 +394,8 @@ __global__ void k_prep(const float* __restrict__ W, int64_t m, int64_t n, int mt
 
 hipError_t launch_prep(hipStream_t s, const float* W, int64_t m, int64_t n, int mt, int nt,
                        float* X, float* Y) {
-    int64_t total = (int64_t)mt * nt * TILE_ELEMS;
-    int64_t g = (total + 255) / 256;
-    if (g > 65535LL * 32) g = 65535LL * 32;
-    hipLaunchKernelGGL(k_prep, dim3((unsigned)g), dim3(256), 0, s, W, m, n, mt, nt, X, Y);
+    hipLaunchKernelGGL(k_prep, dim3((unsigned)((int64_t)mt * nt)), dim3(256), 0, s, W, m, n, mt, nt,
+                       X, Y);
     return hipGetLastError();
 }
 
@@ -367,8 +404,11 @@ hipError_t launch_leaf(hipStream_t s, const LeafArgs& a, int ntiles) {
     return hipGetLastError();
 }
 
-hipError_t launch_node(hipStream_t s, const NodeArgs& a, int gx, int gy) {
-    hipLaunchKernelGGL(k_node, dim3((unsigned)gx, (unsigned)gy, 2), dim3(256), 0, s, a);
+hipError_t launch_node(hipStream_t s, const NodeArgs& a, int nitems, int macro) {
+    if (macro == 4)
+        hipLaunchKernelGGL(k_node<4>, dim3((unsigned)nitems), dim3(256), 0, s, a);
+    else
+        hipLaunchKernelGGL(k_node<2>, dim3((unsigned)nitems), dim3(256), 0, s, a);
     return hipGetLastError();
 }
 
@@ -377,7 +417,8 @@ hipError_t launch_node(hipStream_t s, const NodeArgs& a, int gx, int gy) {
 hipError_t run_schedule(hipStream_t s, const std::vector<SolveOp>& ops, const float* W, int64_t m,
                         int64_t n, int mt, int nt, float* X, float* Y, const float* LA,
                         const float* LB, int b_ident, const float* scale, float qmax,
-                        int8_t* codes, float* V, float* pre, int knear, hipEvent_t* evs) {
+                        int8_t* codes, float* V, float* pre, int knear, const int4* items,
+                        hipEvent_t* evs) {
     if (evs) hipEventRecord(evs[0], s);
     hipError_t e = launch_prep(s, W, m, n, mt, nt, X, Y);
     if (evs) hipEventRecord(evs[1], s);
@@ -406,7 +447,6 @@ hipError_t run_schedule(hipStream_t s, const std::vector<SolveOp>& ops, const fl
     na.Y = Y;
     na.LA = LA;
     na.LB = LB;
-    na.b_ident = b_ident;
     size_t i = 1;
     for (const SolveOp& op : ops) {
         if (evs) hipEventRecord(evs[2 * i], s);
@@ -418,8 +458,8 @@ hipError_t run_schedule(hipStream_t s, const std::vector<SolveOp>& ops, const fl
             na.K = op.K;
             na.Mid = op.Mid;
             na.L = op.L;
-            na.md_lo = op.md_lo;
-            e = launch_node(s, na, op.gx, op.gy);
+            na.items = items + op.item_off;
+            e = launch_node(s, na, op.item_cnt, op.macro);
         }
         if (evs) hipEventRecord(evs[2 * i + 1], s);
         ++i;
