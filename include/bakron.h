@@ -90,9 +90,10 @@ bakron_status bakron_factor(const float *A, int64_t n, const float *B, int64_t m
  *   V      device, m x n fp32 output, V_ij = s_i * codes_ij (one fp32 product)
  *
  * The first call for a given (m, n) allocates the workspace (about 8*m*n
- * bytes) and builds the launch schedule; later calls with the same (m, n)
- * allocate nothing and never synchronise the host.  Kernel faults surface as
- * BAKRON_EHIP on a later call or at the caller's synchronisation.
+ * bytes plus one int per 32 x 32 tile) and builds the launch plan; later
+ * calls with the same (m, n) allocate nothing and never synchronise the host.
+ * All work is enqueued on `stream`.  Kernel faults surface as BAKRON_EHIP on
+ * a later call or at the caller's synchronisation.
  */
 bakron_status bakron_solve(const float *W, int64_t m, int64_t n, const bakron_factors *f,
                            bakron_quantizer q, int8_t *codes, float *V, hipStream_t stream);
@@ -131,17 +132,23 @@ bakron_status bakron_factor_export(const bakron_factors *f, int which, float *ds
 
 /*
  * Measurement hook (not needed for solving).  While enabled, every
- * bakron_solve on the handle records a HIP event pair on its stream around
- * each kernel launch (which adds a few microseconds per launch).  After the
- * caller has synchronised that stream, bakron_profile_read returns, for the
- * last profiled solve, per kernel class:
+ * bakron_solve on the handle records a HIP event pair around each kernel
+ * launch on its stream (which adds a few microseconds per launch).  After the
+ * caller has synchronised that stream, bakron_profile_read fills stats[k] for
+ * the last profiled solve, per kernel class k:
+ *   0 workspace initialisation
+ *   1 segment: rounding of the tiles of a range of tile anti-diagonals
+ *     (Alg. 6 leaves and the lowest recursion levels), near field included
+ *   2 node push: divide-and-conquer band update (Alg. 6 internal nodes)
+ * with
  *   ms          summed launch durations
  *   launches    number of launches
  *   flops       algorithmic work: 2*32^3 flops per (source, target) tile pair
- *               fed back (Eq. (1)), plus the in-tile pairs of the leaves;
- *               for the prep class, bytes moved instead
+ *               fed back (Eq. (1)), plus the in-tile pairs of solved tiles;
+ *               for class 0, bytes moved instead
  *   mfma_flops  flops executed on the matrix cores, zero-masked tiles included
- * Returns BAKRON_EINVAL if no profiled solve has been enqueued since enabling.
+ * Classes beyond nstats are dropped.  Returns BAKRON_EINVAL if no profiled
+ * solve has been enqueued since enabling.
  */
 typedef struct {
     double ms;
@@ -151,8 +158,16 @@ typedef struct {
 } bakron_kernel_stat;
 
 bakron_status bakron_profile_enable(bakron_factors *f, int on);
-bakron_status bakron_profile_read(const bakron_factors *f, bakron_kernel_stat *prep,
-                                  bakron_kernel_stat *leaf, bakron_kernel_stat *node);
+bakron_status bakron_profile_read(const bakron_factors *f, bakron_kernel_stat *stats, int nstats);
+
+/*
+ * bakron_solve_check -- diagnostic (not needed for solving; synchronises
+ * `stream`).  The solve orders the tiles inside one launch with bounded
+ * waits on per-tile ready flags; *failed receives 1 if a wait of the last
+ * solve gave up (its output is then invalid), else 0.  A correct run never
+ * gives up: every awaited tile is held by a running workgroup.
+ */
+bakron_status bakron_solve_check(const bakron_factors *f, hipStream_t stream, int32_t *failed);
 
 #ifdef __cplusplus
 }

@@ -16,7 +16,8 @@ BAKRON_OK, BAKRON_EINVAL, BAKRON_ENOTSPD, BAKRON_ENOMEM, BAKRON_EHIP = range(5)
 
 EXPORTED = ("bakron_factor", "bakron_solve", "bakron_solve_debug", "bakron_factors_free",
             "bakron_status_string", "bakron_factors_error", "bakron_last_error",
-            "bakron_factor_export", "bakron_profile_enable", "bakron_profile_read")
+            "bakron_factor_export", "bakron_profile_enable", "bakron_profile_read",
+            "bakron_solve_check")
 
 _lib = None
 
@@ -70,8 +71,9 @@ def load(path: str = LIB_PATH):
     lib.bakron_profile_enable.restype = ctypes.c_int
     lib.bakron_profile_enable.argtypes = [vp, ctypes.c_int]
     lib.bakron_profile_read.restype = ctypes.c_int
-    lib.bakron_profile_read.argtypes = [vp, ctypes.POINTER(KernelStat), ctypes.POINTER(KernelStat),
-                                        ctypes.POINTER(KernelStat)]
+    lib.bakron_profile_read.argtypes = [vp, ctypes.POINTER(KernelStat), ctypes.c_int]
+    lib.bakron_solve_check.restype = ctypes.c_int
+    lib.bakron_solve_check.argtypes = [vp, vp, ctypes.POINTER(ctypes.c_int32)]
     _lib = lib
     return lib
 
@@ -128,14 +130,25 @@ class Factors:
         if st != BAKRON_OK:
             raise BakronError(st, self.error())
 
+    PROFILE_CLASSES = ("prep", "segment", "node")
+
     def profile_read(self):
         """Per-class stats of the last profiled solve (stream must be synchronised)."""
-        prep, leaf, node = KernelStat(), KernelStat(), KernelStat()
-        st = load().bakron_profile_read(self._h, ctypes.byref(prep), ctypes.byref(leaf),
-                                        ctypes.byref(node))
+        arr = (KernelStat * len(self.PROFILE_CLASSES))()
+        st = load().bakron_profile_read(self._h, arr, len(self.PROFILE_CLASSES))
         if st != BAKRON_OK:
             raise BakronError(st, self.error())
-        return dict(prep=prep.as_dict(), leaf=leaf.as_dict(), node=node.as_dict())
+        return {k: arr[i].as_dict() for i, k in enumerate(self.PROFILE_CLASSES)}
+
+    def check(self) -> bool:
+        """True if the last solve on the current stream completed every
+        ordered wait (synchronises the stream)."""
+        import torch
+        failed = ctypes.c_int32(0)
+        st = load().bakron_solve_check(self._h, _stream(torch, self.device), ctypes.byref(failed))
+        if st != BAKRON_OK:
+            raise BakronError(st, self.error())
+        return failed.value == 0
 
     def close(self):
         if self._h is not None and self._h.value:

@@ -19,11 +19,11 @@ hipError_t factor_one(hipStream_t s, const float* X, int64_t d, double lam, doub
 hipError_t pack_identity(hipStream_t s, int64_t nt, float* packed);
 hipError_t unpack_factor(hipStream_t s, const float* packed, int64_t d, float* dst);
 
-hipError_t run_schedule(hipStream_t s, const std::vector<SolveOp>& ops, const float* W, int64_t m,
-                        int64_t n, int mt, int nt, float* X, float* Y, const float* LA,
-                        const float* LB, int b_ident, const float* scale, float qmax,
-                        int8_t* codes, float* V, float* pre, int knear, const int4* items,
-                        hipEvent_t* evs);
+hipError_t run_plan(hipStream_t st, const Plan& plan, const float* W, int64_t m, int64_t n, int mt,
+                    int nt, const Workspace& ws, const float* LA, const float* LB, int b_ident,
+                    const float* scale, float qmax, int8_t* codes, float* V, float* pre, int knear,
+                    const int4* items, hipEvent_t* tim);
+int plan_timed_launches(const Plan& plan);
 }  // namespace bk
 
 struct bakron_factors {
@@ -36,17 +36,18 @@ struct bakron_factors {
     int64_t LB_tiles = 0;    // tiles per side of LB storage (identity: grown on demand)
     // solve workspace (cached for the last (m, n))
     int64_t ws_m = -1, ws_n = -1;
-    float* X = nullptr;
-    float* Y = nullptr;
+    void* ws_mem = nullptr;         // X, Y tile arrays, flags, counters, status (bk::Workspace)
+    bk::Workspace ws{};
     int knear = 8;
-    std::vector<bk::SolveOp> sched;
-    std::vector<int4> items_host;   // node work lists of the schedule
+    bk::Plan plan;
+    std::vector<int4> items_host;   // node work lists of the plan
     int4* items = nullptr;
-    double prep_bytes = 0.0;
-    // measurement hook
+    // measurement hook: per timed launch (enqueue order) its class and work
     int prof = 0;
     int prof_valid = 0;
-    std::vector<hipEvent_t> evs;
+    std::vector<hipEvent_t> tim;
+    std::vector<int> tclass;        // 0 prep, 1 segment, 2 node
+    std::vector<double> tflops, tmfma;
     std::string err;
 };
 
@@ -84,13 +85,13 @@ static inline int imin(int a, int b) { return a < b ? a : b; }
 
 // Algorithmic flops of one node launch: 2*TS^3 per (source, target) tile
 // pair it pushes, mirroring the kernel's source ranges and masks.
-static double node_alg_flops(const bk::SolveOp& op, int mt, int nt, int knear, int b_ident) {
+static double node_alg_flops(int K, int Mid, int L, int mt, int nt, int knear, int b_ident) {
     double f = 0.0;
-    for (int D = op.Mid; D < op.L; ++D) {
+    for (int D = Mid; D < L; ++D) {
         for (int I = imax(0, D - (nt - 1)); I <= imin(D, mt - 1); ++I) {
             const int J = D - I;
-            if (!b_ident) f += imax(0, imin(op.Mid - J, I - knear) - imax(op.K - J, 0));
-            f += imax(0, imin(op.Mid - I, J - knear) - imax(op.K - I, 0));
+            if (!b_ident) f += imax(0, imin(Mid - J, I - knear) - imax(K - J, 0));
+            f += imax(0, imin(Mid - I, J - knear) - imax(K - I, 0));
         }
     }
     return f * 2.0 * bk::TS * bk::TS * bk::TS;
@@ -132,59 +133,73 @@ static void node_items(int K, int Mid, int L, int mt, int nt, int knear, int b_i
     });
 }
 
-static void build_schedule(int K, int L, int mt, int nt, int knear, int b_ident,
-                           std::vector<bk::SolveOp>& ops, std::vector<int4>& items) {
-    if (L - K == 1) {
-        bk::SolveOp op{};
+static inline int diag_lo(int D, int nt) { return imax(0, D - (nt - 1)); }
+static inline int diag_hi(int D, int mt) { return imin(D, mt - 1); }
+
+// Alg. 6 over tile anti-diagonals [K, L).  A subtree no wider than knear + 1
+// anti-diagonals becomes one persistent segment launch (all its pairs are at
+// distance <= knear and are pulled by their targets); a wider one recurses on
+// [K, Mid), pushes S1 -> S2 for pairs farther apart than knear, then recurses
+// on [Mid, L).  Split at floor((K+L)/2) (App. C: balanced splits).
+static void build_ops(int K, int L, int mt, int nt, int knear, int b_ident, bk::Plan& plan,
+                      std::vector<int4>& items) {
+    const double T = bk::TS, pair = 2.0 * T * T * T;
+    if (L - K <= knear + 1) {
+        bk::PlanOp op{};
         op.kind = 0;
-        op.D = K;
-        op.I_lo = K - (nt - 1) > 0 ? K - (nt - 1) : 0;
-        const int I_hi = K < mt - 1 ? K : mt - 1;
-        op.ntiles = I_hi - op.I_lo + 1;
-        // in-tile pairs: sum over entries of (row + column) predecessors
-        const double T = bk::TS;
-        const double intile = 2.0 * T * T * (T - 1.0);
-        double pushes = 0.0;
-        for (int I = op.I_lo; I <= I_hi; ++I) {
-            const int J = K - I;
-            for (int k = 1; k <= knear; ++k) {
-                if (!b_ident && I + k < mt) pushes += 1.0;
-                if (J + k < nt) pushes += 1.0;
+        op.K = K;
+        op.L = L;
+        double pulls = 0.0;
+        int total = 0;
+        for (int D = K; D < L; ++D)
+            for (int I = diag_lo(D, nt); I <= diag_hi(D, mt); ++I) {
+                const int J = D - I;
+                ++total;
+                if (!b_ident) pulls += imin(I, knear);
+                pulls += imin(J, knear);
             }
-        }
-        op.flops = op.ntiles * intile + pushes * 2.0 * T * T * T;
-        op.mfma_flops = pushes * 2.0 * T * T * T;
-        ops.push_back(op);
+        op.Mid = K;
+        op.strip_lo = imax(0, K - (mt - 1));
+        op.nstrips = imin(nt - 1, L - 1) - op.strip_lo + 1;
+        op.counter = plan.nseg++;
+        op.flops = total * 2.0 * T * T * (T - 1.0) + pulls * pair;   // in-tile pairs + pulls
+        op.mfma_flops = pulls * pair;
+        plan.ops.push_back(op);
         return;
     }
     const int Mid = (K + L) / 2;
-    build_schedule(K, Mid, mt, nt, knear, b_ident, ops, items);
-    if (L - K > knear + 1) {
-        bk::SolveOp op{};
+    build_ops(K, Mid, mt, nt, knear, b_ident, plan, items);
+    int MT = bk::MACRO;
+    std::vector<int4> its;
+    node_items(K, Mid, L, mt, nt, knear, b_ident, 4, its);
+    if ((int)its.size() < 512) {
+        MT = 2;
+        node_items(K, Mid, L, mt, nt, knear, b_ident, 2, its);
+    }
+    if (!its.empty()) {
+        bk::PlanOp op{};
         op.kind = 1;
         op.K = K;
         op.Mid = Mid;
         op.L = L;
-        std::vector<int4> its;
-        // 128 x 128 workgroups when they fill the chip twice over, else 64 x 64
-        op.macro = bk::MACRO;
-        node_items(K, Mid, L, mt, nt, knear, b_ident, 4, its);
-        if ((int)its.size() < 512) {
-            op.macro = 2;
-            node_items(K, Mid, L, mt, nt, knear, b_ident, 2, its);
-        }
-        if (!its.empty()) {
-            op.item_off = (int)items.size();
-            op.item_cnt = (int)its.size();
-            const double chunk = 2.0 * (op.macro * bk::TS) * (op.macro * bk::TS) * bk::TS;
-            op.mfma_flops = 0.0;
-            for (const int4& it : its) op.mfma_flops += (it.w - (it.z >> 1)) * chunk;
-            op.flops = node_alg_flops(op, mt, nt, knear, b_ident);
-            items.insert(items.end(), its.begin(), its.end());
-            ops.push_back(op);
-        }
+        op.macro = MT;
+        op.item_off = (int)items.size();
+        op.item_cnt = (int)its.size();
+        const double chunkf = 2.0 * (MT * T) * (MT * T) * T;
+        for (const int4& it : its) op.mfma_flops += (it.w - (it.z >> 1)) * chunkf;
+        op.flops = node_alg_flops(K, Mid, L, mt, nt, knear, b_ident);
+        items.insert(items.end(), its.begin(), its.end());
+        plan.ops.push_back(op);
     }
-    build_schedule(Mid, L, mt, nt, knear, b_ident, ops, items);
+    build_ops(Mid, L, mt, nt, knear, b_ident, plan, items);
+}
+
+static void build_plan(int mt, int nt, int knear, int b_ident, bk::Plan& plan,
+                       std::vector<int4>& items) {
+    plan.ops.clear();
+    plan.nseg = 0;
+    items.clear();
+    build_ops(0, mt + nt - 1, mt, nt, knear, b_ident, plan, items);
 }
 
 extern "C" bakron_status bakron_factor(const float* A, int64_t n, const float* B, int64_t m,
@@ -207,7 +222,7 @@ extern "C" bakron_status bakron_factor(const float* A, int64_t n, const float* B
     f->damp = damp;
     if (const char* kn = std::getenv("BAKRON_KNEAR")) {
         int v = std::atoi(kn);
-        if (v >= 0 && v <= 8) f->knear = v;
+        if (v >= 0 && v <= bk::KNEAR_MAX) f->knear = v;
     }
 
     const int64_t dmax = (B && m > n) ? m : n;
@@ -291,24 +306,28 @@ extern "C" void bakron_factors_free(bakron_factors* f) {
     hipDeviceSynchronize();
     if (f->LA) hipFree(f->LA);
     if (f->LB) hipFree(f->LB);
-    if (f->X) hipFree(f->X);
-    if (f->Y) hipFree(f->Y);
+    if (f->ws_mem) hipFree(f->ws_mem);
     if (f->items) hipFree(f->items);
-    for (hipEvent_t ev : f->evs) hipEventDestroy(ev);
+    for (hipEvent_t ev : f->tim) hipEventDestroy(ev);
     if (cur != f->device) hipSetDevice(cur);
     delete f;
 }
 
 static bakron_status ensure_workspace(bakron_factors* f, int64_t m, int64_t n) {
-    if (f->ws_m == m && f->ws_n == n && f->X) return BAKRON_OK;
+    if (f->ws_m == m && f->ws_n == n && f->ws_mem) return BAKRON_OK;
     const int64_t mt = cdiv(m, bk::TS), nt = cdiv(n, bk::TS);
-    if (f->X) { hipFree(f->X); f->X = nullptr; }
-    if (f->Y) { hipFree(f->Y); f->Y = nullptr; }
+    if (f->ws_mem) { hipFree(f->ws_mem); f->ws_mem = nullptr; }
     f->ws_m = f->ws_n = -1;
-    const size_t bytes = sizeof(float) * (size_t)mt * (size_t)nt * bk::TILE_ELEMS;
-    hipError_t e = hipMalloc(&f->X, bytes);
-    if (e == hipSuccess) e = hipMalloc(&f->Y, bytes);
+    build_plan((int)mt, (int)nt, f->knear, f->b_ident, f->plan, f->items_host);
+    const size_t tiles = (size_t)mt * (size_t)nt;
+    const size_t fbytes = sizeof(float) * tiles * bk::TILE_ELEMS;
+    const size_t ibytes = sizeof(int) * (tiles + (size_t)f->plan.nseg + 1);
+    hipError_t e = hipMalloc(&f->ws_mem, 2 * fbytes + ibytes);
     if (e != hipSuccess) return hip_fail(&f->err, e, "bakron_solve: hipMalloc (workspace)");
+    char* base = static_cast<char*>(f->ws_mem);
+    int* ints = reinterpret_cast<int*>(base + 2 * fbytes);
+    f->ws = bk::Workspace{reinterpret_cast<float*>(base), reinterpret_cast<float*>(base + fbytes),
+                          ints, ints + tiles, ints + tiles + f->plan.nseg};
     // identity B grows to the requested m
     if (f->b_ident && f->LB_tiles < mt) {
         if (f->LB) hipFree(f->LB);
@@ -319,10 +338,6 @@ static bakron_status ensure_workspace(bakron_factors* f, int64_t m, int64_t n) {
         if (e != hipSuccess) return hip_fail(&f->err, e, "bakron_solve: identity factor");
         f->LB_tiles = mt;
     }
-    f->sched.clear();
-    f->items_host.clear();
-    build_schedule(0, (int)(mt + nt - 1), (int)mt, (int)nt, f->knear, f->b_ident, f->sched,
-                   f->items_host);
     if (f->items) { hipFree(f->items); f->items = nullptr; }
     if (!f->items_host.empty()) {
         const size_t ib = sizeof(int4) * f->items_host.size();
@@ -330,7 +345,15 @@ static bakron_status ensure_workspace(bakron_factors* f, int64_t m, int64_t n) {
         if (e == hipSuccess) e = hipMemcpy(f->items, f->items_host.data(), ib, hipMemcpyHostToDevice);
         if (e != hipSuccess) return hip_fail(&f->err, e, "bakron_solve: work list upload");
     }
-    f->prep_bytes = (double)m * n * 4.0 + 2.0 * 4.0 * mt * nt * bk::TILE_ELEMS;
+    // per timed launch: class and work, in plan order
+    f->tclass.assign(1, 0);
+    f->tflops.assign(1, (double)m * n * 4.0 + 2.0 * (double)fbytes);   // bytes for class 0
+    f->tmfma.assign(1, 0.0);
+    for (const bk::PlanOp& op : f->plan.ops) {
+        f->tclass.push_back(op.kind == 0 ? 1 : 2);
+        f->tflops.push_back(op.flops);
+        f->tmfma.push_back(op.mfma_flops);
+    }
     f->ws_m = m;
     f->ws_n = n;
     return BAKRON_OK;
@@ -362,21 +385,20 @@ static bakron_status solve_impl(const float* W, int64_t m, int64_t n, const bakr
     if (st != BAKRON_OK) return st;
     const int mt = (int)cdiv(m, bk::TS), nt = (int)cdiv(n, bk::TS);
     const float qmax = (float)((1 << (q.bits - 1)) - 1);
-    hipEvent_t* evs = nullptr;
+    hipEvent_t* tim = nullptr;
     f->prof_valid = 0;
     if (f->prof) {
-        const size_t need = 2 * (f->sched.size() + 1);
-        while (f->evs.size() < need) {
+        const size_t need = 2 * (size_t)bk::plan_timed_launches(f->plan);
+        while (f->tim.size() < need) {
             hipEvent_t ev;
             hipError_t ee = hipEventCreate(&ev);
             if (ee != hipSuccess) return hip_fail(&f->err, ee, "bakron_solve: hipEventCreate");
-            f->evs.push_back(ev);
+            f->tim.push_back(ev);
         }
-        evs = f->evs.data();
+        tim = f->tim.data();
     }
-    hipError_t e = bk::run_schedule(stream, f->sched, W, m, n, mt, nt, f->X, f->Y, f->LA, f->LB,
-                                    f->b_ident, q.scale, qmax, codes, V, pre, f->knear, f->items,
-                                    evs);
+    hipError_t e = bk::run_plan(stream, f->plan, W, m, n, mt, nt, f->ws, f->LA, f->LB, f->b_ident,
+                                q.scale, qmax, codes, V, pre, f->knear, f->items, tim);
     if (e != hipSuccess) return hip_fail(&f->err, e, "bakron_solve: launch");
     f->prof_valid = f->prof;
     return BAKRON_OK;
@@ -417,27 +439,36 @@ extern "C" bakron_status bakron_profile_enable(bakron_factors* f, int on) {
     return BAKRON_OK;
 }
 
-extern "C" bakron_status bakron_profile_read(const bakron_factors* f, bakron_kernel_stat* prep,
-                                            bakron_kernel_stat* leaf, bakron_kernel_stat* node) {
-    if (!f || !prep || !leaf || !node) return BAKRON_EINVAL;
+extern "C" bakron_status bakron_profile_read(const bakron_factors* f, bakron_kernel_stat* stats,
+                                            int nstats) {
+    if (!f || !stats || nstats < 1) return BAKRON_EINVAL;
     if (!f->prof_valid) return BAKRON_EINVAL;
-    bakron_kernel_stat* outs[3] = {prep, leaf, node};
-    for (bakron_kernel_stat* o : outs) *o = bakron_kernel_stat{0.0, 0, 0.0, 0.0};
-    float ms = 0.0f;
-    hipError_t e = hipEventElapsedTime(&ms, f->evs[0], f->evs[1]);
-    if (e != hipSuccess) return hip_fail(&const_cast<bakron_factors*>(f)->err, e, "bakron_profile_read");
-    prep->ms = ms;
-    prep->launches = 1;
-    prep->flops = f->prep_bytes;  // bytes moved (the prep kernel does no arithmetic)
-    for (size_t i = 0; i < f->sched.size(); ++i) {
-        e = hipEventElapsedTime(&ms, f->evs[2 * (i + 1)], f->evs[2 * (i + 1) + 1]);
+    for (int k = 0; k < nstats; ++k) stats[k] = bakron_kernel_stat{0.0, 0, 0.0, 0.0};
+    for (size_t i = 0; i < f->tclass.size(); ++i) {
+        float ms = 0.0f;
+        hipError_t e = hipEventElapsedTime(&ms, f->tim[2 * i], f->tim[2 * i + 1]);
         if (e != hipSuccess)
             return hip_fail(&const_cast<bakron_factors*>(f)->err, e, "bakron_profile_read");
-        bakron_kernel_stat* o = f->sched[i].kind == 0 ? leaf : node;
-        o->ms += ms;
-        o->launches += 1;
-        o->flops += f->sched[i].flops;
-        o->mfma_flops += f->sched[i].mfma_flops;
+        const int k = f->tclass[i];
+        if (k >= nstats) continue;
+        stats[k].ms += ms;
+        stats[k].launches += 1;
+        stats[k].flops += f->tflops[i];
+        stats[k].mfma_flops += f->tmfma[i];
     }
+    return BAKRON_OK;
+}
+
+extern "C" bakron_status bakron_solve_check(const bakron_factors* f, hipStream_t stream,
+                                           int32_t* failed) {
+    if (!f || !failed) return BAKRON_EINVAL;
+    bakron_factors* fm = const_cast<bakron_factors*>(f);
+    *failed = 0;
+    if (!f->ws_mem) return BAKRON_OK;
+    int32_t v = 0;
+    hipError_t e = hipMemcpyAsync(&v, f->ws.status, sizeof(v), hipMemcpyDeviceToHost, stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(stream);
+    if (e != hipSuccess) return hip_fail(&fm->err, e, "bakron_solve_check");
+    *failed = v;
     return BAKRON_OK;
 }

@@ -3,16 +3,20 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <vector>
+
 namespace bk {
 
 // Solver tile edge.  The matrix is cut into TS x TS tiles; all tiles on one
 // tile anti-diagonal are mutually independent (App. B: no entry affects an
-// entry on the same or an earlier anti-diagonal), so each leaf launch solves
-// one tile anti-diagonal, one workgroup per tile.
+// entry on the same or an earlier anti-diagonal), and tile (I, J) depends
+// only on tiles (I', J') with I' <= I, J' <= J.
 constexpr int TS = 32;
 constexpr int TILE_ELEMS = TS * TS;
 // Node products use MACRO x MACRO solver tiles per workgroup (128 x 128).
 constexpr int MACRO = 4;
+// Largest supported near-field distance (tiles pulled by the target).
+constexpr int KNEAR_MAX = 8;
 
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
@@ -30,19 +34,45 @@ __host__ __device__ inline int64_t ws_tile_offset(int64_t I, int64_t J, int64_t 
     return (I * nt + J) * (int64_t)TILE_ELEMS;
 }
 
-// One kernel launch of a solve, in stream order.  flops = algorithmic work
-// (2 * TS^3 per (source, target) tile pair, plus the in-tile pairs of a
-// leaf); mfma_flops = what the MFMA units execute including zero-masked
-// operand tiles.
-struct SolveOp {
-    int kind;          // 0 = leaf, 1 = node
-    int D, I_lo, ntiles;
-    int K, Mid, L;
-    int macro;         // node: solver tiles per workgroup edge (4 or 2)
-    int item_off, item_cnt;  // node: slice of the work list
-    double flops;
-    double mfma_flops;
+// Launch plan of one solve shape (Alg. 6 on tile anti-diagonals), all on
+// the caller's stream, in order:
+//   segment : a divide-and-conquer subtree [K, L) no wider than KNEAR + 1
+//             tile anti-diagonals, solved by one persistent launch; each tile
+//             pulls the errors of the tiles at distance 1..KNEAR above it and
+//             to its left itself (Eq. (1)), so every (source, target) pair
+//             closer than KNEAR + 1 is applied by the target;
+//   node    : the push of a wider node, restricted to (source, target) pairs
+//             farther apart than KNEAR, as dense MFMA products.
+// flops = algorithmic work (2 * TS^3 per (source, target) tile pair, plus the
+// in-tile pairs of a solved tile); mfma_flops = executed on the matrix cores,
+// zero-masked tiles included.
+struct PlanOp {
+    int kind;            // 0 segment, 1 node
+    int K, Mid, L;       // segment: diagonals [K, L); node: sources [K, Mid), targets [Mid, L)
+    int strip_lo;        // segment: first tile column (strip) with a tile in [K, L)
+    int nstrips;         // segment: number of such strips
+    int counter;         // segment: index of its ticket counter
+    int macro;           // node: solver tiles per workgroup edge (4 or 2)
+    int item_off, item_cnt;
+    double flops, mfma_flops;
 };
+struct Plan {
+    std::vector<PlanOp> ops;
+    int nseg = 0;
+};
+
+// Solve workspace: X, Y are mt*nt tile arrays of fp32; flags one int per
+// tile; counters one ticket counter per segment; status one int.
+struct Workspace {
+    float* X;
+    float* Y;
+    int* flags;
+    int* counters;
+    int* status;
+};
+
+// Persistent segment launches use at most this many workgroups (one per CU).
+constexpr int SEG_GRID = 256;
 
 // Node work-list item (int4): x = first tile row I0, y = first tile column
 // J0 of the MT x MT macro tile, z = (first source tile << 1) | push kind

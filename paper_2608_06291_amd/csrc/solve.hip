@@ -25,23 +25,27 @@
 // half, solve the second half.  The push of a node is two dense products:
 //     Y[I,J] += sum_{I'} L^B[I,I'] E[I',J]       (same column, I' in S1)
 //     X[I,J] += sum_{J'} F[I,J'] L^A[J,J']^T     (same row,    J' in S1)
-// A leaf solves the tiles of one anti-diagonal and immediately pushes to the
-// KNEAR next tiles below and to the right; node products take only sources
-// farther than KNEAR tiles, so each (source, target) tile pair is applied
-// exactly once.
+// Products between tiles closer than KNEAR + 1 anti-diagonals are pulled by
+// the target tile itself just before it is solved (a persistent "segment"
+// launch covers a subtree of at most KNEAR + 1 anti-diagonals and orders its
+// tiles with per-tile ready flags); node products take only pairs farther
+// apart than KNEAR, so each (source, target) tile pair is applied exactly
+// once.
 #include "common.h"
 
 #include <vector>
 
 namespace bk {
 
-struct LeafArgs {
-    int D;            // tile anti-diagonal
-    int I_lo;         // first tile row on it
+
+struct SegArgs {
+    int K, L;         // tile anti-diagonals [K, L) of this launch
+    int J_lo;         // first tile column (strip) with a tile in [K, L)
+    int nstrips;      // strips J_lo .. J_lo + nstrips - 1
     int mt, nt;       // tile grid
     int64_t m, n;     // real sizes
-    float* X;
-    float* Y;
+    float* X;         // W0 + node row pushes; E once the tile is solved (column-major tiles)
+    float* Y;         // node column pushes; F once the tile is solved (row-major tiles)
     const float* LA;  // packed factor tiles
     const float* LB;
     int b_ident;      // B = I (no column feedback)
@@ -50,169 +54,354 @@ struct LeafArgs {
     int8_t* codes;
     float* V;
     float* pre;       // may be null
-    int knear;
+    int knear;        // pull distances 1..knear (<= KNEAR_MAX)
+    int* flags;       // per tile: 1 once F of the tile is published
+    int* counter;     // strip ticket counter of this launch, 0 at entry
+    int* status;      // set to 1 if a wait gave up (never in a correct run)
 };
 
-// One workgroup (1024 threads) per tile.  Thread <-> entry (p, q); wave w
-// holds the entries with (p + q) mod 32 in {2w, 2w+1}, so the entries of one
-// element anti-diagonal d are all in one wave (half of it).
+// Bounded wait for a tile's ready flag, executed by a whole wave (uniform
+// address).  A strip only ever waits for strips with smaller tickets, and
+// tickets are handed out only to running workgroups, so the flag is set by a
+// running workgroup; the bound only turns a logic error into a reported
+// failure instead of a hang.  The data behind the flag is read with
+// device-coherent (sc1) loads, so no cache invalidation is needed here.
+constexpr int SPIN_LIMIT = 1 << 22;
+__device__ inline void wait_ready(const int* flag, int* status) {
+    int it = 0;
+    while (__hip_atomic_load(flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0) {
+        __builtin_amdgcn_s_sleep(1);
+        if (++it >= SPIN_LIMIT ||
+            __hip_atomic_load(status, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0) {
+            __hip_atomic_store(status, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            break;
+        }
+    }
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);   // keep the data loads after the wait
+}
+
+// Raw buffer descriptor over one 32 x 32 fp32 tile (16-byte loads).
+__device__ inline __amdgpu_buffer_rsrc_t tile_rsrc(const float* t) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(t), (short)0, TILE_ELEMS * 4,
+                                             0x00020000);
+}
+constexpr int CPOL_SC1 = 16;   // device-coherent load / store
+
+// Pulled contributions of one source tile at distance k, on fp32 MFMA
+// (C[M][N] += sum_k A[M][k] B[k][N]; lane half h takes k = 16h + s at step
+// s, so each lane reads 16 consecutive floats of each operand):
+//   row pull (target X-type):    C[q][p] += sum_j L^A[J, J-k][q][j] F[I, J-k][p][j]
+//     A = factor tile rows, B column p = row p of F (row-major Y tile of the
+//     strip to the left, published inside this launch: sc1 loads);
+//   column pull (target Y-type): C[p][q] += sum_i L^B[I, I-k][p][i] E[I-k, J][i][q]
+//     B column q = column q of E, kept transposed in the strip's LDS ring.
+__device__ inline void mfma_16(const f32x4* a4, const f32x4* b4, f32x16& acc) {
+#pragma unroll
+    for (int st = 0; st < 16; ++st)
+        acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a4[st >> 2][st & 3], b4[st >> 2][st & 3], acc,
+                                                    0, 0, 0);
+}
+
+constexpr int RING = KNEAR_MAX;   // E tiles of the strip kept in LDS
+constexpr int RSTR = TS + 4;      // ring row stride: 16-byte rows, conflict-free b128 reads
+
+// Persistent solve of the tiles on anti-diagonals [K, L) by tile-column
+// strips.  Each workgroup (512 threads, one per CU) repeatedly takes a strip
+// ticket and solves the strip's tiles in [K, L) top to bottom; strip J waits
+// only for strips J-1 .. J-knear, which hold smaller tickets.  Inside a strip
+// the column dependencies are local: the last RING errors E of the strip stay
+// in LDS.  Per tile:
+//  1. pull: waves 0-3 the row contributions of tiles (I, J-k) (wave 0:
+//     distance 1, the critical one; waves 1-3: distances 2..knear), each wave
+//     waiting for its source tile's flag; waves 4-7 the column contributions
+//     of tiles (I-k, J) from the ring.  Partial sums meet in LDS and are
+//     added in a fixed order (deterministic);
+//  2. in-tile rounding of the 63 element anti-diagonals (below);
+//  3. publish F -> Y (sc1 stores), wait for them, set the tile's flag; E goes
+//     to the ring and to X (read by the node launches after this one); then
+//     codes, V and pre.
 //
-// Per step d: the owners of diagonal d quantise and publish the error E of
-// their column and the F of their row; every thread then adds one column
-// push (L^B[p][d-q] * E[d-q][q]) and one row push (F[p][d-p] * L^A[q][d-p]).
-// The coefficients are held in registers, each thread's factor row rotated so
-// that step d reads register (d mod 32): no dynamic register indexing.
-__global__ __launch_bounds__(1024) void k_leaf(LeafArgs a) {
+// In-tile rounding: each thread owns two entries of one row p: slot 0 at
+// column q0 and slot 1 at column q1 = q0 + 1 (mod 32), so p + q1 = p + q0 + 1.
+// Half-wave h of wave w owns the rows' entries whose anti-diagonal index is
+// {4w + 2h, 4w + 2h + 1} mod 32: two consecutive element anti-diagonals d
+// (slot 0) and d + 1 (slot 1) are handled by the same half-wave, one barrier
+// per pair.  Within a pair, the only feedback from diagonal d into d + 1 is
+// the error of the entry just above (row p - 1, same column: one lane down,
+// DPP wave_shr:1) through L^B[p][p-1], and the F of the entry just to the
+// left (the thread's own slot 0) through L^A[q1][q0] (Eq. (1) restricted to
+// the two diagonals).  After the barrier every thread adds the column pushes
+// L^B[p][i] * E[i][q] and row pushes F[p][j] * L^A[q][j] of both diagonals to
+// both of its entries.  Coefficients are register-resident, each factor row
+// rotated so that step d reads register (d mod 32).
+__global__ __launch_bounds__(512) void k_seg(SegArgs a) {
     __shared__ float LBt[TS][TS];            // unpadded: the rotated reads below are conflict-free
     __shared__ float LAt[TS][TS];
-    __shared__ float Et[TS][TS + 1];
-    __shared__ float Ft[TS][TS + 1];
-    __shared__ float Pw[16][TS][TS + 1];     // per-wave push factor tile (prefetched)
-    __shared__ float Ow[16][TILE_ELEMS];     // per-wave push target tile, fragment order (prefetched)
-    __shared__ float Ecol[2][TS];
-    __shared__ float Frow[2][TS];
+    __shared__ float Ecs[2][2][2 * TS];      // [buffer][diagonal of the pair][column (+ dummies)]
+    __shared__ float2 Frs[2][2 * TS];        // [buffer][row (+ dummies)] = (F on d, F on d + 1)
+    __shared__ float Red[8][TS][TS + 1];     // pulled partial sums, one slice per wave
+    __shared__ __attribute__((aligned(16))) float Ering[RING][TS][RSTR];   // E^T[q][i] per tile
+    __shared__ int tk;
 
-    const int I = a.I_lo + (int)blockIdx.x;
-    const int J = a.D - I;
     const int tid = threadIdx.x;
     const int w = tid >> 6, l = tid & 63;
-    const int c = 2 * w + (l >> 5);
+    const int hf = l >> 5;
     const int p = l & 31;
-    const int q = (c - p) & 31;
+    const int c0 = 4 * w + 2 * hf;
+    const int q0 = (c0 - p) & 31;
+    const int q1 = (q0 + 1) & 31;
     const int lr = l & 31, lk = l >> 5;
+    const float qmax = a.qmax;
+    const int knear = a.knear;
 
-    // Near push of this wave: target kk = w/2 + 1 tiles below (even w, column
-    // push into Y) or to the right (odd w, row push into X).  The factor tile
-    // and the target tile do not change during this launch, so both are
-    // fetched now and the push at the end touches no global memory before its
-    // final store.
-    const int kk = (w >> 1) + 1;
-    const bool colpush = (w & 1) == 0;
-    int TI = I, TJ = J;
-    bool active = kk <= a.knear;
-    const float* fac = nullptr;
-    if (colpush) {
-        TI = I + kk;
-        active = active && !a.b_ident && TI < a.mt;
-        if (active) fac = a.LB + packed_tile_offset(TI, I);
-    } else {
-        TJ = J + kk;
-        active = active && TJ < a.nt;
-        if (active) fac = a.LA + packed_tile_offset(TJ, J);
-    }
-    float* out = colpush ? a.Y : a.X;
-    const int64_t to = ws_tile_offset(TI, TJ, a.nt);
-    if (active) {
-#pragma unroll
-        for (int s4 = 0; s4 < 4; ++s4) {
-            const int e0 = (s4 * 64 + l) * 4;
-            const f32x4 v = *reinterpret_cast<const f32x4*>(fac + e0);
-            const int r = e0 >> 5, cc = e0 & 31;
-            Pw[w][r][cc] = v[0];
-            Pw[w][r][cc + 1] = v[1];
-            Pw[w][r][cc + 2] = v[2];
-            Pw[w][r][cc + 3] = v[3];
+    for (;;) {
+        if (tid == 0) tk = atomicAdd(a.counter, 1);
+        __syncthreads();
+        const int sidx = tk;
+        if (sidx >= a.nstrips) break;   // uniform
+        const int J = a.J_lo + sidx;
+        const int I_first = a.K - J > 0 ? a.K - J : 0;
+        const int I_last = a.L - 1 - J < a.mt - 1 ? a.L - 1 - J : a.mt - 1;
+
+        // strip set-up: L^A[J, J], the ring with the errors of the tiles above
+        // that were solved by earlier launches
+        for (int e = tid; e < TILE_ELEMS; e += 512) LAt[e >> 5][e & 31] = a.LA[packed_tile_offset(J, J) + e];
+        if (!a.b_ident) {
+            const int npre = knear < I_first ? knear : I_first;
+            for (int k = 1; k <= npre; ++k) {
+                const float* src = a.X + ws_tile_offset(I_first - k, J, a.nt);   // E^T, column-major E
+                float (*ring)[RSTR] = Ering[(I_first - k) % RING];
+                for (int e = tid; e < TILE_ELEMS; e += 512) ring[e >> 5][e & 31] = src[e];
+            }
         }
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-            const int rr = (r >> 2) * 8 + lk * 4 + (r & 3);
-            Ow[w][r * 64 + l] = out[to + rr * TS + lr];
+        __syncthreads();
+
+        // inputs of the first tile; later tiles' inputs are prefetched during
+        // the previous tile's rounding loop
+        float pf_lb0, pf_lb1, pf_h0, pf_h1, pf_g0, pf_g1, pf_s;
+        {
+            const int64_t tb = ws_tile_offset(I_first, J, a.nt);
+            const float* lbp = a.LB + packed_tile_offset(I_first, I_first);
+            pf_lb0 = a.b_ident ? 0.0f : lbp[tid];
+            pf_lb1 = a.b_ident ? 0.0f : lbp[tid + 512];
+            pf_h0 = a.X[tb + q0 * TS + p];
+            pf_h1 = a.X[tb + q1 * TS + p];
+            pf_g0 = a.Y[tb + p * TS + q0];
+            pf_g1 = a.Y[tb + p * TS + q1];
+            const int row = I_first * TS + p;
+            pf_s = row < a.m ? a.scale[row] : 0.0f;
         }
-    }
 
-    {   // diagonal factor tiles
-        const int r = tid >> 5, cc = tid & 31;
-        LAt[r][cc] = a.LA[packed_tile_offset(J, J) + tid];
-        LBt[r][cc] = a.b_ident ? (r == cc ? 1.0f : 0.0f) : a.LB[packed_tile_offset(I, I) + tid];
-    }
-    const int64_t tbase = ws_tile_offset(I, J, a.nt);
-    const int64_t xo = tbase + q * TS + p;     // X tiles are column-major
-    const int64_t yo = tbase + p * TS + q;     // Y tiles are row-major
-    float h = a.X[xo];
-    float g = a.Y[yo];
-    const int64_t row = (int64_t)I * TS + p, col = (int64_t)J * TS + q;
-    const float s = (row < a.m) ? a.scale[row] : 0.0f;
-    const float inv_s = (s > 0.0f) ? 1.0f / s : 0.0f;
-    __syncthreads();
-
-    float lbr[TS], lar[TS];
+        for (int I = I_first; I <= I_last; ++I) {
+            // lane constants are recomputed per tile from an opaque copy of the
+            // thread index, so the compiler does not keep every derived LDS
+            // address of the unrolled loop below live across tiles
+            int tid = threadIdx.x;
+            asm volatile("" : "+v"(tid));
+            const int w = (int)threadIdx.x >> 6, l = tid & 63;   // w: wave-uniform
+            const int hf = l >> 5;
+            const int p = l & 31;
+            const int c0 = 4 * w + 2 * hf;
+            const int q0 = (c0 - p) & 31;
+            const int q1 = (q0 + 1) & 31;
+            const int lr = l & 31, lk = l >> 5;
+            const int64_t tbase = ws_tile_offset(I, J, a.nt);
+            float* const Xg = a.X + tbase;   // X tile: column-major
+            float* const Yg = a.Y + tbase;   // Y tile: row-major
+            {
+                const int e0 = tid, e1 = tid + 512;   // LBt rows e >> 5, columns e & 31
+                LBt[e0 >> 5][e0 & 31] = a.b_ident ? ((e0 >> 5) == (e0 & 31) ? 1.0f : 0.0f) : pf_lb0;
+                LBt[e1 >> 5][e1 & 31] = a.b_ident ? ((e1 >> 5) == (e1 & 31) ? 1.0f : 0.0f) : pf_lb1;
+            }
+            float h0 = pf_h0, h1 = pf_h1;
+            float g0 = pf_g0, g1 = pf_g1;
+            const int row = I * TS + p;
+            const float s = pf_s;
+            const float inv_s = (s > 0.0f) ? 1.0f / s : 0.0f;
+            __syncthreads();   // LBt, and the ring entry of the previous tile
+            float lbr[TS], lar0[TS], lar1[TS];
 #pragma unroll
-    for (int k = 0; k < TS; ++k) {
-        lbr[k] = LBt[p][(k - q) & 31];
-        lar[k] = LAt[q][(k - p) & 31];
-    }
+            for (int k = 0; k < TS; ++k) { lbr[k] = LBt[p][(k - q0) & 31]; lar0[k] = LAt[q0][(k - p) & 31]; lar1[k] = LAt[q1][(k - p) & 31]; }
 
-    float e_out = 0.0f, f_out = 0.0f, x_out = __builtin_nanf("");
-    int c_out = 0;
-    for (int d0 = 0; d0 < 2 * TS; d0 += TS) {
+            // 1. pull distances 1..knear (knear <= 8).  Waves 0-3 (row kind)
+            // and 4-7 (column kind) each take one K quarter of the distance-1
+            // product (the critical one: 4 MFMAs per wave) and up to two of the
+            // products of distances 2..knear (wave quarter wi: 2 + wi, 6 + wi).
+            // All loads of a wave are issued before its first MFMA.  Row
+            // sources of distance >= 2 are complete once tile (I, J-2) is:
+            // every tile waits for its left neighbour before it starts, so one
+            // flag stands for the whole row to its left.
+            {
+                const bool rowkind = w < 4;
+                const int wi = w & 3;
+                const int rofs = lr * TS + lk * 16;
+                f32x16 acc = {0};
+                if (rowkind) {
+                    const bool v1 = knear >= 1 && J >= 1;
+                    f32x4 a1;
+                    if (v1)
+                        a1 = *reinterpret_cast<const f32x4*>(a.LA + packed_tile_offset(J, J - 1) + rofs + 4 * wi);
+                    if (2 + wi <= knear && J - 2 - wi >= 0) {
+                        wait_ready(a.flags + I * a.nt + (J - 2), a.status);
+                        for (int k = 2 + wi; k <= knear && J - k >= 0; k += 4) {
+                            f32x4 a4[4], b4[4];
+                            const f32x4* fa = reinterpret_cast<const f32x4*>(a.LA + packed_tile_offset(J, J - k) + rofs);
+                            const __amdgpu_buffer_rsrc_t rb = tile_rsrc(a.Y + ws_tile_offset(I, J - k, a.nt));
 #pragma unroll
-        for (int k = 0; k < TS; ++k) {
-            if (w == (k >> 1) && (l >> 5) == (k & 1)) {
-                const bool valid = (p + q == d0 + k);
-                const float acc = g + h;
-                float e = 0.0f, f = 0.0f;
-                if (valid) {
-                    float x, v;
-                    int cc;
-                    if (s > 0.0f) {
-                        x = acc * inv_s;
-                        float r = rintf(x);
-                        r = fminf(fmaxf(r, -a.qmax), a.qmax);
-                        cc = (int)r;
-                        v = r * s;
-                    } else {
-                        x = __builtin_nanf("");
-                        cc = 0;
-                        v = 0.0f;
+                            for (int v = 0; v < 4; ++v) {
+                                a4[v] = fa[v];
+                                b4[v] = __builtin_amdgcn_raw_buffer_load_b128(rb, (rofs + 4 * v) * 4, 0, CPOL_SC1);
+                            }
+                            mfma_16(a4, b4, acc);
+                        }
                     }
-                    e = v - acc;
-                    f = g + e;
-                    e_out = e;
-                    f_out = f;
-                    x_out = x;
-                    c_out = cc;
+                    if (v1) {   // distance 1, K quarter wi: k = 16 lk + 4 wi + s
+                        wait_ready(a.flags + I * a.nt + (J - 1), a.status);
+                        const __amdgpu_buffer_rsrc_t r1 = tile_rsrc(a.Y + ws_tile_offset(I, J - 1, a.nt));
+                        const f32x4 b1 = __builtin_amdgcn_raw_buffer_load_b128(r1, (rofs + 4 * wi) * 4, 0, CPOL_SC1);
+#pragma unroll
+                        for (int st = 0; st < 4; ++st)
+                            acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a1[st], b1[st], acc, 0, 0, 0);
+                    }
+                } else if (!a.b_ident) {
+                    if (knear >= 1 && I >= 1) {
+                        const f32x4 a1 = *reinterpret_cast<const f32x4*>(
+                            a.LB + packed_tile_offset(I, I - 1) + rofs + 4 * wi);
+                        const f32x4 b1 = *reinterpret_cast<const f32x4*>(&Ering[(I - 1) % RING][lr][lk * 16 + 4 * wi]);
+#pragma unroll
+                        for (int st = 0; st < 4; ++st)
+                            acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a1[st], b1[st], acc, 0, 0, 0);
+                    }
+                    for (int k = 2 + wi; k <= knear && I - k >= 0; k += 4) {
+                        f32x4 a4[4], b4[4];
+                        const f32x4* fa = reinterpret_cast<const f32x4*>(a.LB + packed_tile_offset(I, I - k) + rofs);
+                        const float* rb = &Ering[(I - k) % RING][lr][lk * 16];
+#pragma unroll
+                        for (int v = 0; v < 4; ++v) {
+                            a4[v] = fa[v];
+                            b4[v] = *reinterpret_cast<const f32x4*>(rb + 4 * v);
+                        }
+                        mfma_16(a4, b4, acc);
+                    }
                 }
-                Ecol[k & 1][q] = e;
-                Frow[k & 1][p] = f;
+#pragma unroll
+                for (int r = 0; r < 16; ++r) Red[w][(r >> 2) * 8 + lk * 4 + (r & 3)][lr] = acc[r];
             }
             __syncthreads();
-            const float ein = Ecol[k & 1][q];
-            const float fin = Frow[k & 1][p];
-            g = fmaf(lbr[k], ein, g);
-            h = fmaf(fin, lar[k], h);
-        }
-    }
-
-    a.X[xo] = e_out;
-    a.Y[yo] = f_out;
-    if (row < a.m && col < a.n) {
-        const int64_t o = row * a.n + col;
-        a.codes[o] = (int8_t)c_out;
-        a.V[o] = (float)c_out * s;
-        if (a.pre) a.pre[o] = x_out;
-    }
-    Et[p][q] = e_out;
-    Ft[p][q] = f_out;
-    __syncthreads();
-
-    if (!active) return;   // wave-uniform; no barrier follows
-    f32x16 acc = {0};
 #pragma unroll
-    for (int k0 = 0; k0 < TS; k0 += 2) {
-        float av, bv;
-        if (colpush) {            // Y[TI, J] += L^B[TI, I] (32x32) * E (32x32)
-            av = Pw[w][lr][k0 + lk];
-            bv = Et[k0 + lk][lr];
-        } else {                  // X[I, TJ]^T += L^A[TJ, J] * F^T (X is column-major)
-            av = Pw[w][lr][k0 + lk];
-            bv = Ft[lr][k0 + lk];
-        }
-        acc = __builtin_amdgcn_mfma_f32_32x32x2f32(av, bv, acc, 0, 0, 0);
-    }
+            for (int v = 0; v < 4; ++v) {
+                h0 += Red[v][q0][p];
+                h1 += Red[v][q1][p];
+                g0 += Red[4 + v][p][q0];
+                g1 += Red[4 + v][p][q1];
+            }
+
+            if (I < I_last) {   // prefetch the next tile's inputs (consumed after the loop)
+                const int In = I + 1;
+                const int64_t tb = ws_tile_offset(In, J, a.nt);
+                const float* lbp = a.LB + packed_tile_offset(In, In);
+                if (!a.b_ident) {
+                    pf_lb0 = lbp[tid];
+                    pf_lb1 = lbp[tid + 512];
+                }
+                pf_h0 = a.X[tb + q0 * TS + p];
+                pf_h1 = a.X[tb + q1 * TS + p];
+                pf_g0 = a.Y[tb + p * TS + q0];
+                pf_g1 = a.Y[tb + p * TS + q1];
+                const int rn = In * TS + p;
+                pf_s = rn < a.m ? a.scale[rn] : 0.0f;
+            }
+
+            // 2. in-tile rounding.  Quantisation without branches: a zero scale
+            // gives inv_s = 0, so x = 0, code 0, V = 0 and E = -W~ (the row's
+            // alphabet is {0}).  Each thread keeps E, F and x of its own two
+            // entries when it processes them.
+            float eo0 = 0.0f, eo1 = 0.0f, fo0 = 0.0f, fo1 = 0.0f, xv0 = 0.0f, xv1 = 0.0f;
+            for (int d0 = 0; d0 < 2 * TS; d0 += TS) {
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-        const int rr = (r >> 2) * 8 + lk * 4 + (r & 3);
-        out[to + rr * TS + lr] = Ow[w][r * 64 + l] + acc[r];
+                for (int kp = 0; kp < TS; kp += 2) {
+                    const int d = d0 + kp;
+                    const int buf = (kp >> 1) & 1;
+                    if (w == (kp >> 2)) {                       // wave-uniform
+                        const bool act = hf == ((kp >> 1) & 1);
+                        // slot 0: anti-diagonal d
+                        const bool v0 = act && (p + q0 == d);
+                        const float acc0 = g0 + h0;
+                        const float x0 = acc0 * inv_s;
+                        const float r0 = __builtin_amdgcn_fmed3f(rintf(x0), -qmax, qmax);
+                        const float ew0 = fmaf(r0, s, -acc0);
+                        const float e0 = v0 ? ew0 : 0.0f;
+                        const float f0 = v0 ? g0 + ew0 : 0.0f;
+                        // slot 1: anti-diagonal d + 1, plus the two pushes from d
+                        const float eup = __int_as_float(
+                            __builtin_amdgcn_update_dpp(0, __float_as_int(e0), 0x138, 0xf, 0xf, true));
+                        const float g1n = fmaf(lbr[(kp - 1) & 31], eup, g1);
+                        const float h1n = fmaf(f0, lar1[kp & 31], h1);
+                        const bool v1 = act && (p + q1 == d + 1);
+                        const float acc1 = g1n + h1n;
+                        const float x1 = acc1 * inv_s;
+                        const float r1 = __builtin_amdgcn_fmed3f(rintf(x1), -qmax, qmax);
+                        const float ew1 = fmaf(r1, s, -acc1);
+                        const float e1 = v1 ? ew1 : 0.0f;
+                        const float f1 = v1 ? g1n + ew1 : 0.0f;
+                        // broadcast to every thread (inactive half writes the dummy slots)
+                        Ecs[buf][0][act ? q0 : TS + p] = e0;
+                        Ecs[buf][1][act ? q1 : TS + p] = e1;
+                        Frs[buf][act ? p : TS + p] = make_float2(f0, f1);
+                        // keep the processed entries' outputs
+                        eo0 = v0 ? e0 : eo0;
+                        fo0 = v0 ? f0 : fo0;
+                        xv0 = v0 ? x0 : xv0;
+                        eo1 = v1 ? e1 : eo1;
+                        fo1 = v1 ? f1 : fo1;
+                        xv1 = v1 ? x1 : xv1;
+                    }
+                    __syncthreads();
+                    const float ea0 = Ecs[buf][0][q0], ea1 = Ecs[buf][0][q1];
+                    const float eb0 = Ecs[buf][1][q0], eb1 = Ecs[buf][1][q1];
+                    const float2 fr = Frs[buf][p];
+                    g0 = fmaf(lbr[kp & 31], ea0, g0);
+                    g0 = fmaf(lbr[(kp + 1) & 31], eb0, g0);
+                    g1 = fmaf(lbr[(kp - 1) & 31], ea1, g1);
+                    g1 = fmaf(lbr[kp & 31], eb1, g1);
+                    h0 = fmaf(fr.x, lar0[kp & 31], h0);
+                    h0 = fmaf(fr.y, lar0[(kp + 1) & 31], h0);
+                    h1 = fmaf(fr.x, lar1[kp & 31], h1);
+                    h1 = fmaf(fr.y, lar1[(kp + 1) & 31], h1);
+                }
+            }
+
+            // 3. publish F (device-coherent), then the flag; E to the ring and X
+            __hip_atomic_store(Yg + p * TS + q0, fo0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_store(Yg + p * TS + q1, fo1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            Xg[q0 * TS + p] = eo0;
+            Xg[q1 * TS + p] = eo1;
+            Ering[I % RING][q0][p] = eo0;
+            Ering[I % RING][q1][p] = eo1;
+            __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0): this wave's stores are complete
+            __syncthreads();
+            if (tid == 0)
+                __hip_atomic_store(a.flags + I * a.nt + J, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+
+            const int64_t col0 = (int64_t)J * TS + q0, col1 = (int64_t)J * TS + q1;
+            const float nan = __builtin_nanf("");
+            if (row < a.m) {
+                if (col0 < a.n) {
+                    const int64_t o = (int64_t)row * a.n + col0;
+                    const float r = __builtin_amdgcn_fmed3f(rintf(xv0), -qmax, qmax);
+                    a.codes[o] = (int8_t)(int)r;
+                    a.V[o] = r * s;
+                    if (a.pre) a.pre[o] = s > 0.0f ? xv0 : nan;
+                }
+                if (col1 < a.n) {
+                    const int64_t o = (int64_t)row * a.n + col1;
+                    const float r = __builtin_amdgcn_fmed3f(rintf(xv1), -qmax, qmax);
+                    a.codes[o] = (int8_t)(int)r;
+                    a.V[o] = r * s;
+                    if (a.pre) a.pre[o] = s > 0.0f ? xv1 : nan;
+                }
+            }
+        }
     }
 }
 
@@ -360,12 +549,15 @@ __global__ __launch_bounds__(256, (MT == 4 ? 2 : 4)) void k_node(NodeArgs a) {
         }
 }
 
-// X <- W (tile-major, column-major inside each tile, zero padding), Y <- 0.
-// One workgroup per tile; the transpose goes through LDS so that both the
-// read of W and the write of X are coalesced.
+// X <- W (tile-major, column-major inside each tile, zero padding), Y <- 0,
+// ready flags <- 0 and ticket counters <- 0.  One workgroup per tile; the
+// transpose goes through LDS so that both the read of W and the write of X
+// are coalesced.
 __global__ __launch_bounds__(256) void k_prep(const float* __restrict__ W, int64_t m, int64_t n,
                                               int mt, int nt, float* __restrict__ X,
-                                              float* __restrict__ Y) {
+                                              float* __restrict__ Y, int* __restrict__ flags,
+                                              int* __restrict__ counters, int ncounters,
+                                              int* __restrict__ status) {
     __shared__ float T[TS][TS + 1];
     const int64_t tile = blockIdx.x;
     const int64_t I = tile / nt, J = tile - (tile / nt) * nt;
@@ -378,94 +570,73 @@ __global__ __launch_bounds__(256) void k_prep(const float* __restrict__ W, int64
         T[r][c] = (gr < m && gc < n) ? W[gr * n + gc] : 0.0f;
     }
     __syncthreads();
-    float* x = X + tile * TILE_ELEMS;
-    float* y = Y + tile * TILE_ELEMS;
+    const int64_t base = tile * TILE_ELEMS;
 #pragma unroll
     for (int k = 0; k < TILE_ELEMS / 256; ++k) {
         const int e = k * 256 + tid;
         const int c = e >> 5, r = e & 31;
-        x[e] = T[r][c];
-        y[e] = 0.0f;
+        X[base + e] = T[r][c];
+        Y[base + e] = 0.0f;
+    }
+    if (tid == 0) flags[tile] = 0;
+    if (tile == 0) {
+        for (int i = tid; i < ncounters; i += 256) counters[i] = 0;
+        if (tid == 0) *status = 0;
     }
 }
 
 // ---------------------------------------------------------------------------
-// host launchers
+// host launch driver
 
-hipError_t launch_prep(hipStream_t s, const float* W, int64_t m, int64_t n, int mt, int nt,
-                       float* X, float* Y) {
-    hipLaunchKernelGGL(k_prep, dim3((unsigned)((int64_t)mt * nt)), dim3(256), 0, s, W, m, n, mt, nt,
-                       X, Y);
-    return hipGetLastError();
-}
+// Launches the plan on one stream.  tim (optional, profiling): an event pair
+// around every launch, in plan order (prep first).
+hipError_t run_plan(hipStream_t st, const Plan& plan, const float* W, int64_t m, int64_t n, int mt,
+                    int nt, const Workspace& ws, const float* LA, const float* LB, int b_ident,
+                    const float* scale, float qmax, int8_t* codes, float* V, float* pre, int knear,
+                    const int4* items, hipEvent_t* tim) {
+    int ti = 0;
+    auto t_begin = [&]() { if (tim) hipEventRecord(tim[2 * ti], st); };
+    auto t_end = [&]() { if (tim) hipEventRecord(tim[2 * ti + 1], st); ++ti; };
+    hipError_t e;
+    t_begin();
+    hipLaunchKernelGGL(k_prep, dim3((unsigned)((int64_t)mt * nt)), dim3(256), 0, st, W, m, n, mt, nt,
+                       ws.X, ws.Y, ws.flags, ws.counters, plan.nseg, ws.status);
+    t_end();
+    if ((e = hipGetLastError()) != hipSuccess) return e;
 
-hipError_t launch_leaf(hipStream_t s, const LeafArgs& a, int ntiles) {
-    hipLaunchKernelGGL(k_leaf, dim3((unsigned)ntiles), dim3(1024), 0, s, a);
-    return hipGetLastError();
-}
-
-hipError_t launch_node(hipStream_t s, const NodeArgs& a, int nitems, int macro) {
-    if (macro == 4)
-        hipLaunchKernelGGL(k_node<4>, dim3((unsigned)nitems), dim3(256), 0, s, a);
-    else
-        hipLaunchKernelGGL(k_node<2>, dim3((unsigned)nitems), dim3(256), 0, s, a);
-    return hipGetLastError();
-}
-
-// Enqueue a whole solve.  evs (optional): 2 * (ops.size() + 1) events; a pair
-// is recorded around the prep launch and around every schedule launch.
-hipError_t run_schedule(hipStream_t s, const std::vector<SolveOp>& ops, const float* W, int64_t m,
-                        int64_t n, int mt, int nt, float* X, float* Y, const float* LA,
-                        const float* LB, int b_ident, const float* scale, float qmax,
-                        int8_t* codes, float* V, float* pre, int knear, const int4* items,
-                        hipEvent_t* evs) {
-    if (evs) hipEventRecord(evs[0], s);
-    hipError_t e = launch_prep(s, W, m, n, mt, nt, X, Y);
-    if (evs) hipEventRecord(evs[1], s);
-    if (e != hipSuccess) return e;
-    LeafArgs la{};
-    la.mt = mt;
-    la.nt = nt;
-    la.m = m;
-    la.n = n;
-    la.X = X;
-    la.Y = Y;
-    la.LA = LA;
-    la.LB = LB;
-    la.b_ident = b_ident;
-    la.scale = scale;
-    la.qmax = qmax;
-    la.codes = codes;
-    la.V = V;
-    la.pre = pre;
-    la.knear = knear;
-    NodeArgs na{};
-    na.knear = knear;
-    na.mt = mt;
-    na.nt = nt;
-    na.X = X;
-    na.Y = Y;
-    na.LA = LA;
-    na.LB = LB;
-    size_t i = 1;
-    for (const SolveOp& op : ops) {
-        if (evs) hipEventRecord(evs[2 * i], s);
+    SegArgs sa{};
+    sa.mt = mt; sa.nt = nt; sa.m = m; sa.n = n; sa.X = ws.X; sa.Y = ws.Y;
+    sa.LA = LA; sa.LB = LB; sa.b_ident = b_ident; sa.scale = scale; sa.qmax = qmax;
+    sa.codes = codes; sa.V = V; sa.pre = pre; sa.knear = knear; sa.flags = ws.flags;
+    sa.status = ws.status;
+    NodeArgs nd{};
+    nd.knear = knear; nd.mt = mt; nd.nt = nt; nd.X = ws.X; nd.Y = ws.Y; nd.LA = LA; nd.LB = LB;
+    for (const PlanOp& op : plan.ops) {
+        t_begin();
         if (op.kind == 0) {
-            la.D = op.D;
-            la.I_lo = op.I_lo;
-            e = launch_leaf(s, la, op.ntiles);
+            sa.K = op.K;
+            sa.L = op.L;
+            sa.J_lo = op.strip_lo;
+            sa.nstrips = op.nstrips;
+            sa.counter = ws.counters + op.counter;
+            const int grid = op.nstrips < SEG_GRID ? op.nstrips : SEG_GRID;
+            hipLaunchKernelGGL(k_seg, dim3((unsigned)grid), dim3(512), 0, st, sa);
         } else {
-            na.K = op.K;
-            na.Mid = op.Mid;
-            na.L = op.L;
-            na.items = items + op.item_off;
-            e = launch_node(s, na, op.item_cnt, op.macro);
+            nd.K = op.K;
+            nd.Mid = op.Mid;
+            nd.L = op.L;
+            nd.items = items + op.item_off;
+            if (op.macro == 4)
+                hipLaunchKernelGGL(k_node<4>, dim3((unsigned)op.item_cnt), dim3(256), 0, st, nd);
+            else
+                hipLaunchKernelGGL(k_node<2>, dim3((unsigned)op.item_cnt), dim3(256), 0, st, nd);
         }
-        if (evs) hipEventRecord(evs[2 * i + 1], s);
-        ++i;
-        if (e != hipSuccess) return e;
+        t_end();
+        if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     return hipSuccess;
 }
+
+int plan_timed_launches(const Plan& plan) { return 1 + (int)plan.ops.size(); }
 
 }  // namespace bk

@@ -65,6 +65,7 @@ def gpu_run(p, debug=True, k=None, repeat=1):
         pre = torch.full(W.shape, float("nan"), dtype=torch.float32, device=dev) if debug else None
         r = pk.solve(W, f, p["bits"], s, codes=codes, V=V, pre=pre, debug=debug)
         torch.cuda.synchronize()
+        assert f.check(), "a tile-ordering wait of the solve gave up"
         outs.append(tuple(None if t is None else t.cpu().numpy() for t in
                           (r[0], r[1], r[2] if debug else None)))
     f.close()

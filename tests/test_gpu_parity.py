@@ -26,10 +26,12 @@ def test_parity_shapes(oracle_mod, m, n):
     check_against_oracle(p, codes, V, pre, oracle_mod, label=f"shape{m}x{n}")
 
 
-@pytest.mark.parametrize("k", [0, 1, 3])
+@pytest.mark.parametrize("k", [0, 1, 3, 8])
 @pytest.mark.parametrize("m,n", [(200, 300), (300, 200), (161, 161)])
 def test_parity_node_paths(oracle_mod, m, n, k):
-    """Small KNEAR sends most tile pairs through the divide-and-conquer nodes."""
+    """Small KNEAR sends most tile pairs through the divide-and-conquer nodes
+    (KNEAR 0: every segment is one tile anti-diagonal and nothing is pulled);
+    KNEAR 8 is the largest near field the segment kernel supports."""
     p = _problem(m, n, seed=7 + m + n)
     log(f"case node-path m={m} n={n} knear={k}")
     codes, V, pre = gpu_run(p, k=k)
