@@ -137,8 +137,8 @@ constexpr int RSTR = TS + 4;      // ring row stride: 16-byte rows, conflict-fre
 __global__ __launch_bounds__(512) void k_seg(SegArgs a) {
     __shared__ float LBt[TS][TS];            // unpadded: the rotated reads below are conflict-free
     __shared__ float LAt[TS][TS];
-    __shared__ float Ecs[2][2][2 * TS];      // [buffer][diagonal of the pair][column (+ dummies)]
-    __shared__ float2 Frs[2][2 * TS];        // [buffer][row (+ dummies)] = (F on d, F on d + 1)
+    __shared__ float Ecs[2][2][2][2 * TS];   // [turn parity][round][diagonal of the pair][column (+ dummies)]
+    __shared__ float2 Frs[2][2][2 * TS];     // [turn parity][round][row (+ dummies)] = (F on d, F on d + 1)
     __shared__ float Red[8][TS][TS + 1];     // pulled partial sums, one slice per wave
     __shared__ __attribute__((aligned(16))) float Ering[RING][TS][RSTR];   // E^T[q][i] per tile
     __shared__ int tk;
@@ -317,57 +317,76 @@ __global__ __launch_bounds__(512) void k_seg(SegArgs a) {
             // alphabet is {0}).  Each thread keeps E, F and x of its own two
             // entries when it processes them.
             float eo0 = 0.0f, eo1 = 0.0f, fo0 = 0.0f, fo1 = 0.0f, xv0 = 0.0f, xv1 = 0.0f;
+            // one round: the active half-wave quantises anti-diagonals d and d + 1
+            // and broadcasts their E (per column) and F (per row) through LDS
+            auto round = [&](int kp, int d, int tp, int rb) {
+                const bool act = hf == ((kp >> 1) & 1);
+                // slot 0: anti-diagonal d
+                const bool v0 = act && (p + q0 == d);
+                const float acc0 = g0 + h0;
+                const float x0 = acc0 * inv_s;
+                const float r0 = __builtin_amdgcn_fmed3f(rintf(x0), -qmax, qmax);
+                const float ew0 = fmaf(r0, s, -acc0);
+                const float e0 = v0 ? ew0 : 0.0f;
+                const float f0 = v0 ? g0 + ew0 : 0.0f;
+                // slot 1: anti-diagonal d + 1, plus the two pushes from d
+                const float eup = __int_as_float(
+                    __builtin_amdgcn_update_dpp(0, __float_as_int(e0), 0x138, 0xf, 0xf, true));
+                const float g1n = fmaf(lbr[(kp - 1) & 31], eup, g1);
+                const float h1n = fmaf(f0, lar1[kp & 31], h1);
+                const bool v1 = act && (p + q1 == d + 1);
+                const float acc1 = g1n + h1n;
+                const float x1 = acc1 * inv_s;
+                const float r1 = __builtin_amdgcn_fmed3f(rintf(x1), -qmax, qmax);
+                const float ew1 = fmaf(r1, s, -acc1);
+                const float e1 = v1 ? ew1 : 0.0f;
+                const float f1 = v1 ? g1n + ew1 : 0.0f;
+                // broadcast (the inactive half writes the dummy slots)
+                Ecs[tp][rb][0][act ? q0 : TS + p] = e0;
+                Ecs[tp][rb][1][act ? q1 : TS + p] = e1;
+                Frs[tp][rb][act ? p : TS + p] = make_float2(f0, f1);
+                // keep the processed entries' outputs
+                eo0 = v0 ? e0 : eo0;
+                fo0 = v0 ? f0 : fo0;
+                xv0 = v0 ? x0 : xv0;
+                eo1 = v1 ? e1 : eo1;
+                fo1 = v1 ? f1 : fo1;
+                xv1 = v1 ? x1 : xv1;
+            };
+            // every thread adds the pushes of one round to both of its entries
+            auto update = [&](int kp, int tp, int rb) {
+                const float ea0 = Ecs[tp][rb][0][q0], ea1 = Ecs[tp][rb][0][q1];
+                const float eb0 = Ecs[tp][rb][1][q0], eb1 = Ecs[tp][rb][1][q1];
+                const float2 fr = Frs[tp][rb][p];
+                g0 = fmaf(lbr[kp & 31], ea0, g0);
+                g0 = fmaf(lbr[(kp + 1) & 31], eb0, g0);
+                g1 = fmaf(lbr[(kp - 1) & 31], ea1, g1);
+                g1 = fmaf(lbr[kp & 31], eb1, g1);
+                h0 = fmaf(fr.x, lar0[kp & 31], h0);
+                h0 = fmaf(fr.y, lar0[(kp + 1) & 31], h0);
+                h1 = fmaf(fr.x, lar1[kp & 31], h1);
+                h1 = fmaf(fr.y, lar1[(kp + 1) & 31], h1);
+            };
+            // Wave kq owns anti-diagonals 4kq .. 4kq + 3 (mod 32): two rounds in a
+            // row (its half 0, then its half 1).  Between them only that wave
+            // needs the first round's values, so it reads them back itself (LDS
+            // operations of one wave complete in order) and the workgroup
+            // barrier comes once per turn of two rounds.  Buffers alternate
+            // with the turn's parity, so a turn never overwrites values that a
+            // slower wave may still be reading from the previous turn.
             for (int d0 = 0; d0 < 2 * TS; d0 += TS) {
 #pragma unroll
-                for (int kp = 0; kp < TS; kp += 2) {
-                    const int d = d0 + kp;
-                    const int buf = (kp >> 1) & 1;
-                    if (w == (kp >> 2)) {                       // wave-uniform
-                        const bool act = hf == ((kp >> 1) & 1);
-                        // slot 0: anti-diagonal d
-                        const bool v0 = act && (p + q0 == d);
-                        const float acc0 = g0 + h0;
-                        const float x0 = acc0 * inv_s;
-                        const float r0 = __builtin_amdgcn_fmed3f(rintf(x0), -qmax, qmax);
-                        const float ew0 = fmaf(r0, s, -acc0);
-                        const float e0 = v0 ? ew0 : 0.0f;
-                        const float f0 = v0 ? g0 + ew0 : 0.0f;
-                        // slot 1: anti-diagonal d + 1, plus the two pushes from d
-                        const float eup = __int_as_float(
-                            __builtin_amdgcn_update_dpp(0, __float_as_int(e0), 0x138, 0xf, 0xf, true));
-                        const float g1n = fmaf(lbr[(kp - 1) & 31], eup, g1);
-                        const float h1n = fmaf(f0, lar1[kp & 31], h1);
-                        const bool v1 = act && (p + q1 == d + 1);
-                        const float acc1 = g1n + h1n;
-                        const float x1 = acc1 * inv_s;
-                        const float r1 = __builtin_amdgcn_fmed3f(rintf(x1), -qmax, qmax);
-                        const float ew1 = fmaf(r1, s, -acc1);
-                        const float e1 = v1 ? ew1 : 0.0f;
-                        const float f1 = v1 ? g1n + ew1 : 0.0f;
-                        // broadcast to every thread (inactive half writes the dummy slots)
-                        Ecs[buf][0][act ? q0 : TS + p] = e0;
-                        Ecs[buf][1][act ? q1 : TS + p] = e1;
-                        Frs[buf][act ? p : TS + p] = make_float2(f0, f1);
-                        // keep the processed entries' outputs
-                        eo0 = v0 ? e0 : eo0;
-                        fo0 = v0 ? f0 : fo0;
-                        xv0 = v0 ? x0 : xv0;
-                        eo1 = v1 ? e1 : eo1;
-                        fo1 = v1 ? f1 : fo1;
-                        xv1 = v1 ? x1 : xv1;
+                for (int kq = 0; kq < 8; ++kq) {
+                    const int tp = kq & 1, kpa = 4 * kq, kpb = 4 * kq + 2;
+                    if (w == kq) {                       // wave-uniform
+                        round(kpa, d0 + kpa, tp, 0);
+                        __builtin_amdgcn_wave_barrier();
+                        update(kpa, tp, 0);
+                        round(kpb, d0 + kpb, tp, 1);
                     }
                     __syncthreads();
-                    const float ea0 = Ecs[buf][0][q0], ea1 = Ecs[buf][0][q1];
-                    const float eb0 = Ecs[buf][1][q0], eb1 = Ecs[buf][1][q1];
-                    const float2 fr = Frs[buf][p];
-                    g0 = fmaf(lbr[kp & 31], ea0, g0);
-                    g0 = fmaf(lbr[(kp + 1) & 31], eb0, g0);
-                    g1 = fmaf(lbr[(kp - 1) & 31], ea1, g1);
-                    g1 = fmaf(lbr[kp & 31], eb1, g1);
-                    h0 = fmaf(fr.x, lar0[kp & 31], h0);
-                    h0 = fmaf(fr.y, lar0[(kp + 1) & 31], h0);
-                    h1 = fmaf(fr.x, lar1[kp & 31], h1);
-                    h1 = fmaf(fr.y, lar1[(kp + 1) & 31], h1);
+                    if (w != kq) update(kpa, tp, 0);
+                    update(kpb, tp, 1);
                 }
             }
 
