@@ -78,6 +78,22 @@ def cpu_baseline(cfg_inputs, seconds: float) -> dict:
                 host_nproc=os.cpu_count())
 
 
+def measured_traffic(kernel: str, workload: str):
+    """HBM bytes per launch from the committed rocprofv3 FETCH_SIZE/WRITE_SIZE
+    summary, or None if there is none for this kernel and workload or the
+    kernel sources changed since it was measured."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", f"{kernel}_{workload}_hbm-traffic.json")
+    if not os.path.exists(path):
+        return None
+    rec = json.load(open(path))
+    src = b"".join(open(os.path.join(ROOT, "paper_2608_06291_amd", "csrc", f), "rb").read()
+                   for f in ("solve.hip", "common.h"))
+    if hashlib.sha256(src).hexdigest() != rec.get("source_sha256"):
+        return None
+    return rec["bytes_per_launch"]
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -88,6 +104,9 @@ def main():
     ap.add_argument("--profile-steps", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--copy-calibration-mib", type=int, default=0,
+                    help="only run a plain device-to-device copy of this many MiB (10 times) and "
+                         "exit: the reference for scaling rocprofv3 FETCH_SIZE/WRITE_SIZE counters")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: --gpus {args.gpus} is not supported: the BaKron solve runs on one "
@@ -97,6 +116,16 @@ def main():
 
     import numpy as np
     import torch
+
+    if args.copy_calibration_mib > 0:
+        nbytes = args.copy_calibration_mib << 20
+        src = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda:0")
+        dst = torch.empty_like(src)
+        for _ in range(10):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"[bench] copied {nbytes} bytes 10 times")
+        return
 
     import paper_2608_06291_amd as pk
     import workloads
@@ -179,7 +208,8 @@ def main():
     if dominant == "segment":
         roof = dict(kernel="k_seg (persistent tile-wavefront rounding with near-field pulls)",
                     bound="alu", achieved=tf["segment"], peak=PEAK_FP32_VALU, unit="TFLOP/s",
-                    frac=tf["segment"] / PEAK_FP32_VALU, traffic=None)
+                    frac=tf["segment"] / PEAK_FP32_VALU,
+                    traffic=measured_traffic("k_seg", cfg.name))
     else:
         roof = dict(kernel="k_node (divide-and-conquer band push), fp32 MFMA", bound="mfma",
                     achieved=tf["node"], peak=PEAK_FP32_MFMA, unit="TFLOP/s",
