@@ -87,39 +87,64 @@ __device__ inline __amdgpu_buffer_rsrc_t tile_rsrc(const float* t) {
 }
 constexpr int CPOL_SC1 = 16;   // device-coherent load / store
 
-// Pulled contributions of one source tile at distance k, on fp32 MFMA
-// (C[M][N] += sum_k A[M][k] B[k][N]; lane half h takes k = 16h + s at step
-// s, so each lane reads 16 consecutive floats of each operand):
-//   row pull (target X-type):    C[q][p] += sum_j L^A[J, J-k][q][j] F[I, J-k][p][j]
-//     A = factor tile rows, B column p = row p of F (row-major Y tile of the
-//     strip to the left, published inside this launch: sc1 loads);
-//   column pull (target Y-type): C[p][q] += sum_i L^B[I, I-k][p][i] E[I-k, J][i][q]
-//     B column q = column q of E, kept transposed in the strip's LDS ring.
-__device__ inline void mfma_16(const f32x4* a4, const f32x4* b4, f32x16& acc) {
+// Near-field pulls on fp32 MFMA (v_mfma_f32_16x16x4f32).  The pulled sums of
+// a tile are two 32 x 32 products per source distance k:
+//   row kind    (into X): C[q][p] += sum_j L^A[J, J-k][q][j] F[I, J-k][p][j]
+//   column kind (into Y): C[p][q] += sum_i L^B[I, I-k][p][i] E[I-k, J][i][q]
+// Waves 0-3 own one 16 x 16 block of the row-kind C each, waves 4-7 one block
+// of the column-kind C, so no partial sums have to be combined.  Every
+// operand is read as contiguous 16-byte chunks of a row: lane (i, s) of a
+// 16 x 16 x 4 step supplies A[i][k] and B[k][i] with k = 8s + 4c + t at step
+// (c, t), i.e. chunks 2s and 2s + 1 of row i of both operand tiles.
+//
+// Factor tiles and the left strips' F tiles are staged in LDS with direct
+// global -> LDS loads (no registers in flight), 16-byte chunk c of row r at
+// chunk c ^ (r & 7) so that the row-per-lane reads above spread over the banks.
+__device__ inline f32x4 lds_chunk(const float* t, int r, int c) {
+    return *reinterpret_cast<const f32x4*>(t + r * TS + ((c ^ (r & 7)) << 2));
+}
+__device__ inline void mfma_8(f32x4 a0, f32x4 a1, f32x4 b0, f32x4 b1, f32x4& acc) {
 #pragma unroll
-    for (int st = 0; st < 16; ++st)
-        acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a4[st >> 2][st & 3], b4[st >> 2][st & 3], acc,
-                                                    0, 0, 0);
+    for (int t = 0; t < 4; ++t) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a0[t], b0[t], acc, 0, 0, 0);
+#pragma unroll
+    for (int t = 0; t < 4; ++t) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a1[t], b1[t], acc, 0, 0, 0);
+}
+// One wave copies rows 8 rb .. 8 rb + 7 of a row-major tile into a swizzled
+// LDS tile: lane l fills physical chunk l & 7 of row 8 rb + (l >> 3).
+template <int CPOL>
+__device__ inline void stage_rows(const float* src, float* dst, int rb, int l) {
+    const int r = 8 * rb + (l >> 3), c = (l & 7) ^ (r & 7);
+    __builtin_amdgcn_global_load_lds(src + r * TS + 4 * c,
+                                     (__attribute__((address_space(3))) void*)(dst + rb * 256), 16,
+                                     0, CPOL);
 }
 
 constexpr int RING = KNEAR_MAX;   // E tiles of the strip kept in LDS
 constexpr int RSTR = TS + 4;      // ring row stride: 16-byte rows, conflict-free b128 reads
+constexpr int PULL_T0 = 2;        // first loop turn whose idle waves may consume staged operands
 
 // Persistent solve of the tiles on anti-diagonals [K, L) by tile-column
 // strips.  Each workgroup (512 threads, one per CU) repeatedly takes a strip
 // ticket and solves the strip's tiles in [K, L) top to bottom; strip J waits
-// only for strips J-1 .. J-knear, which hold smaller tickets.  Inside a strip
-// the column dependencies are local: the last RING errors E of the strip stay
-// in LDS.  Per tile:
-//  1. pull: waves 0-3 the row contributions of tiles (I, J-k) (wave 0:
-//     distance 1, the critical one; waves 1-3: distances 2..knear), each wave
-//     waiting for its source tile's flag; waves 4-7 the column contributions
-//     of tiles (I-k, J) from the ring.  Partial sums meet in LDS and are
-//     added in a fixed order (deterministic);
+// only for strips J-1 .. J-2, which hold smaller tickets.  Inside a strip the
+// column dependencies are local: the last RING errors E of the strip stay in
+// LDS, and so do L^A[J, J-k] for k = 1..knear.  Per tile I:
+//  1. pull.  The sources at distance k >= 2 of tile I are complete while
+//     tile I-1 is being rounded (tile (I, J-2) finished before tile (I-1, J)
+//     started, and every tile waits for its left neighbour, so one flag
+//     stands for the whole row to its left).  Their operands are staged in
+//     LDS at the start of tile I-1's rounding loop and the waves multiply them
+//     in the loop turns in which they are idle; what remains (the first tile
+//     of a strip, or a left strip that was late) is done here, followed by
+//     distance 1: the row source (I, J-1) after its ready flag (device-
+//     coherent loads) and the column source E(I-1) from the ring.  The 16 x 16
+//     blocks meet in LDS;
 //  2. in-tile rounding of the 63 element anti-diagonals (below);
-//  3. publish F -> Y (sc1 stores), wait for them, set the tile's flag; E goes
-//     to the ring and to X (read by the node launches after this one); then
-//     codes, V and pre.
+//  3. publish F -> Y: the tile is gathered in LDS and written as whole
+//     128-byte rows with device-coherent (sc1) 16-byte stores, which the
+//     memory system acknowledges much sooner than scattered 4-byte ones; wait
+//     for them, set the tile's flag.  E goes to the ring and to X (read by the
+//     node launches after this one); then codes, V and pre.
 //
 // In-tile rounding: each thread owns two entries of one row p: slot 0 at
 // column q0 and slot 1 at column q1 = q0 + 1 (mod 32), so p + q1 = p + q0 + 1.
@@ -139,9 +164,14 @@ __global__ __launch_bounds__(512) void k_seg(SegArgs a) {
     __shared__ float LAt[TS][TS];
     __shared__ float Ecs[2][2][2][2 * TS];   // [turn parity][round][diagonal of the pair][column (+ dummies)]
     __shared__ float2 Frs[2][2][2 * TS];     // [turn parity][round][row (+ dummies)] = (F on d, F on d + 1)
-    __shared__ float Red[8][TS][TS + 1];     // pulled partial sums, one slice per wave
+    __shared__ float HR[TS][TS + 1];         // pulled row-kind sum, [q][p]
+    __shared__ float GC[TS][TS + 1];         // pulled column-kind sum, [p][q]
     __shared__ __attribute__((aligned(16))) float Ering[RING][TS][RSTR];   // E^T[q][i] per tile
-    __shared__ int tk;
+    __shared__ __attribute__((aligned(16))) float LAs[KNEAR_MAX][TILE_ELEMS];      // L^A[J, J-k-1]
+    __shared__ __attribute__((aligned(16))) float LBn[KNEAR_MAX][TILE_ELEMS];      // L^B[I', I'-k-1]
+    __shared__ __attribute__((aligned(16))) float Yn[KNEAR_MAX - 1][TILE_ELEMS];   // F[I', J-k-2]
+    __shared__ __attribute__((aligned(16))) float Fst[TS][RSTR];   // F of the tile, row-major
+    __shared__ int tk, ynext;
 
     const int tid = threadIdx.x;
     const int w = tid >> 6, l = tid & 63;
@@ -150,9 +180,9 @@ __global__ __launch_bounds__(512) void k_seg(SegArgs a) {
     const int c0 = 4 * w + 2 * hf;
     const int q0 = (c0 - p) & 31;
     const int q1 = (q0 + 1) & 31;
-    const int lr = l & 31, lk = l >> 5;
     const float qmax = a.qmax;
     const int knear = a.knear;
+    const bool roww = w < 4;   // wave-uniform: row-kind or column-kind pull blocks
 
     for (;;) {
         if (tid == 0) tk = atomicAdd(a.counter, 1);
@@ -162,10 +192,14 @@ __global__ __launch_bounds__(512) void k_seg(SegArgs a) {
         const int J = a.J_lo + sidx;
         const int I_first = a.K - J > 0 ? a.K - J : 0;
         const int I_last = a.L - 1 - J < a.mt - 1 ? a.L - 1 - J : a.mt - 1;
+        const int kr = knear < J ? knear : J;   // row sources k = 1..kr of every tile of the strip
+        const bool need_y = kr >= 2;
 
-        // strip set-up: L^A[J, J], the ring with the errors of the tiles above
-        // that were solved by earlier launches
+        // strip set-up: L^A[J, J] and L^A[J, J-k], the ring with the errors of
+        // the tiles above that were solved by earlier launches
         for (int e = tid; e < TILE_ELEMS; e += 512) LAt[e >> 5][e & 31] = a.LA[packed_tile_offset(J, J) + e];
+        for (int g = w; g < 4 * kr; g += 8)
+            stage_rows<0>(a.LA + packed_tile_offset(J, J - 1 - (g >> 2)), LAs[g >> 2], g & 3, l);
         if (!a.b_ident) {
             const int npre = knear < I_first ? knear : I_first;
             for (int k = 1; k <= npre; ++k) {
@@ -192,6 +226,12 @@ __global__ __launch_bounds__(512) void k_seg(SegArgs a) {
             pf_s = row < a.m ? a.scale[row] : 0.0f;
         }
 
+        // pull state of the next tile (uniform): which operands are staged,
+        // and per wave the next source distance to multiply
+        bool lb_staged = false, y_staged = false;
+        int nk = 2;
+        f32x4 pacc = {0.0f, 0.0f, 0.0f, 0.0f};
+
         for (int I = I_first; I <= I_last; ++I) {
             // lane constants are recomputed per tile from an opaque copy of the
             // thread index, so the compiler does not keep every derived LDS
@@ -204,7 +244,11 @@ __global__ __launch_bounds__(512) void k_seg(SegArgs a) {
             const int c0 = 4 * w + 2 * hf;
             const int q0 = (c0 - p) & 31;
             const int q1 = (q0 + 1) & 31;
-            const int lr = l & 31, lk = l >> 5;
+            const int i16 = l & 15, ks = l >> 4;
+            // pull block of this wave: A-operand rows ra0 + i16, B-operand rows rb
+            const int ra0 = roww ? 16 * (w >> 1) : 16 * ((w - 4) >> 1);
+            const int rb = (roww ? 16 * (w & 1) : 16 * ((w - 4) & 1)) + i16;
+            const int ra = ra0 + i16;
             const int64_t tbase = ws_tile_offset(I, J, a.nt);
             float* const Xg = a.X + tbase;   // X tile: column-major
             float* const Yg = a.Y + tbase;   // Y tile: row-major
@@ -218,85 +262,93 @@ __global__ __launch_bounds__(512) void k_seg(SegArgs a) {
             const int row = I * TS + p;
             const float s = pf_s;
             const float inv_s = (s > 0.0f) ? 1.0f / s : 0.0f;
-            __syncthreads();   // LBt, and the ring entry of the previous tile
-            float lbr[TS], lar0[TS], lar1[TS];
-#pragma unroll
-            for (int k = 0; k < TS; ++k) { lbr[k] = LBt[p][(k - q0) & 31]; lar0[k] = LAt[q0][(k - p) & 31]; lar1[k] = LAt[q1][(k - p) & 31]; }
+            const int kc = a.b_ident ? 0 : (knear < I ? knear : I);   // column sources k = 1..kc
 
-            // 1. pull distances 1..knear (knear <= 8).  Waves 0-3 (row kind)
-            // and 4-7 (column kind) each take one K quarter of the distance-1
-            // product (the critical one: 4 MFMAs per wave) and up to two of the
-            // products of distances 2..knear (wave quarter wi: 2 + wi, 6 + wi).
-            // All loads of a wave are issued before its first MFMA.  Row
-            // sources of distance >= 2 are complete once tile (I, J-2) is:
-            // every tile waits for its left neighbour before it starts, so one
-            // flag stands for the whole row to its left.
+            // multiplies source distance k of tile It into pacc (row or column kind)
+            auto pull_src = [&](int It, int k) {
+                f32x4 a0, a1, b0, b1;
+                if (roww) {
+                    a0 = lds_chunk(LAs[k - 1], ra, 2 * ks);
+                    a1 = lds_chunk(LAs[k - 1], ra, 2 * ks + 1);
+                    b0 = lds_chunk(Yn[k - 2], rb, 2 * ks);
+                    b1 = lds_chunk(Yn[k - 2], rb, 2 * ks + 1);
+                } else {
+                    const float* e = &Ering[(It - k) % RING][rb][8 * ks];
+                    a0 = lds_chunk(LBn[k - 1], ra, 2 * ks);
+                    a1 = lds_chunk(LBn[k - 1], ra, 2 * ks + 1);
+                    b0 = *reinterpret_cast<const f32x4*>(e);
+                    b1 = *reinterpret_cast<const f32x4*>(e + 4);
+                }
+                mfma_8(a0, a1, b0, b1, pacc);
+            };
+            // issues the direct loads of tile It's operands: L^B[It, It-k],
+            // k = 1..min(knear, It), and F[It, J-k], k = 2..kr
+            auto stage = [&](int It, bool lb, bool y) {
+                const int nlb = lb ? (knear < It ? knear : It) : 0;
+                const int ny = y ? kr - 1 : 0;
+                for (int g = w; g < 4 * (nlb + ny); g += 8) {
+                    const int ti = g >> 2;
+                    if (ti < nlb)
+                        stage_rows<0>(a.LB + packed_tile_offset(It, It - 1 - ti), LBn[ti], g & 3, l);
+                    else
+                        stage_rows<CPOL_SC1>(a.Y + ws_tile_offset(It, J - 2 - (ti - nlb), a.nt),
+                                             Yn[ti - nlb], g & 3, l);
+                }
+            };
+
+            // 1. pull.  Operands not staged during the previous tile's loop
+            // (first tile of the strip, or a left strip that was late) are
+            // staged now.
+            const bool lb_need = !a.b_ident && kc >= 1;
+            if ((lb_need && !lb_staged) || (need_y && !y_staged) || I == I_first) {   // uniform
+                if (need_y && !y_staged) wait_ready(a.flags + I * a.nt + (J - 2), a.status);
+                stage(I, lb_need && !lb_staged, need_y && !y_staged);
+                __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0): this wave's direct loads landed
+                __syncthreads();
+            }
             {
-                const bool rowkind = w < 4;
-                const int wi = w & 3;
-                const int rofs = lr * TS + lk * 16;
-                f32x16 acc = {0};
-                if (rowkind) {
-                    const bool v1 = knear >= 1 && J >= 1;
-                    f32x4 a1;
-                    if (v1)
-                        a1 = *reinterpret_cast<const f32x4*>(a.LA + packed_tile_offset(J, J - 1) + rofs + 4 * wi);
-                    if (2 + wi <= knear && J - 2 - wi >= 0) {
-                        wait_ready(a.flags + I * a.nt + (J - 2), a.status);
-                        for (int k = 2 + wi; k <= knear && J - k >= 0; k += 4) {
-                            f32x4 a4[4], b4[4];
-                            const f32x4* fa = reinterpret_cast<const f32x4*>(a.LA + packed_tile_offset(J, J - k) + rofs);
-                            const __amdgpu_buffer_rsrc_t rb = tile_rsrc(a.Y + ws_tile_offset(I, J - k, a.nt));
-#pragma unroll
-                            for (int v = 0; v < 4; ++v) {
-                                a4[v] = fa[v];
-                                b4[v] = __builtin_amdgcn_raw_buffer_load_b128(rb, (rofs + 4 * v) * 4, 0, CPOL_SC1);
-                            }
-                            mfma_16(a4, b4, acc);
-                        }
-                    }
-                    if (v1) {   // distance 1, K quarter wi: k = 16 lk + 4 wi + s
+                const int kmax = roww ? kr : kc;
+                for (; nk <= kmax; ++nk) pull_src(I, nk);
+                if (roww) {
+                    if (kr >= 1) {   // distance 1: F[I, J-1] straight from memory after its flag
                         wait_ready(a.flags + I * a.nt + (J - 1), a.status);
                         const __amdgpu_buffer_rsrc_t r1 = tile_rsrc(a.Y + ws_tile_offset(I, J - 1, a.nt));
-                        const f32x4 b1 = __builtin_amdgcn_raw_buffer_load_b128(r1, (rofs + 4 * wi) * 4, 0, CPOL_SC1);
-#pragma unroll
-                        for (int st = 0; st < 4; ++st)
-                            acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a1[st], b1[st], acc, 0, 0, 0);
+                        const f32x4 b0 = __builtin_amdgcn_raw_buffer_load_b128(r1, (rb * TS + 8 * ks) * 4, 0, CPOL_SC1);
+                        const f32x4 b1 = __builtin_amdgcn_raw_buffer_load_b128(r1, (rb * TS + 8 * ks + 4) * 4, 0, CPOL_SC1);
+                        mfma_8(lds_chunk(LAs[0], ra, 2 * ks), lds_chunk(LAs[0], ra, 2 * ks + 1), b0, b1, pacc);
                     }
-                } else if (!a.b_ident) {
-                    if (knear >= 1 && I >= 1) {
-                        const f32x4 a1 = *reinterpret_cast<const f32x4*>(
-                            a.LB + packed_tile_offset(I, I - 1) + rofs + 4 * wi);
-                        const f32x4 b1 = *reinterpret_cast<const f32x4*>(&Ering[(I - 1) % RING][lr][lk * 16 + 4 * wi]);
-#pragma unroll
-                        for (int st = 0; st < 4; ++st)
-                            acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a1[st], b1[st], acc, 0, 0, 0);
-                    }
-                    for (int k = 2 + wi; k <= knear && I - k >= 0; k += 4) {
-                        f32x4 a4[4], b4[4];
-                        const f32x4* fa = reinterpret_cast<const f32x4*>(a.LB + packed_tile_offset(I, I - k) + rofs);
-                        const float* rb = &Ering[(I - k) % RING][lr][lk * 16];
-#pragma unroll
-                        for (int v = 0; v < 4; ++v) {
-                            a4[v] = fa[v];
-                            b4[v] = *reinterpret_cast<const f32x4*>(rb + 4 * v);
-                        }
-                        mfma_16(a4, b4, acc);
-                    }
+                } else if (kc >= 1) {   // distance 1: E[I-1, J] from the ring
+                    const float* e = &Ering[(I - 1) % RING][rb][8 * ks];
+                    mfma_8(lds_chunk(LBn[0], ra, 2 * ks), lds_chunk(LBn[0], ra, 2 * ks + 1),
+                           *reinterpret_cast<const f32x4*>(e), *reinterpret_cast<const f32x4*>(e + 4), pacc);
                 }
+                float (*out)[TS + 1] = roww ? HR : GC;
 #pragma unroll
-                for (int r = 0; r < 16; ++r) Red[w][(r >> 2) * 8 + lk * 4 + (r & 3)][lr] = acc[r];
+                for (int r = 0; r < 4; ++r) out[ra0 + 4 * ks + r][rb] = pacc[r];
             }
+            if (tid == 0)   // can the next tile's row operands be staged during this tile's loop?
+                ynext = (need_y && I < I_last)
+                            ? __hip_atomic_load(a.flags + (I + 1) * a.nt + (J - 2), __ATOMIC_RELAXED,
+                                                __HIP_MEMORY_SCOPE_AGENT)
+                            : 0;
             __syncthreads();
-#pragma unroll
-            for (int v = 0; v < 4; ++v) {
-                h0 += Red[v][q0][p];
-                h1 += Red[v][q1][p];
-                g0 += Red[4 + v][p][q0];
-                g1 += Red[4 + v][p][q1];
+            h0 += HR[q0][p];
+            h1 += HR[q1][p];
+            g0 += GC[p][q0];
+            g1 += GC[p][q1];
+            pacc = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+            nk = 2;
+            const bool has_next = I < I_last;
+            const int kc_next = a.b_ident ? 0 : (knear < I + 1 ? knear : I + 1);
+            lb_staged = has_next;
+            y_staged = has_next && ynext != 0;
+            if (has_next) {
+                __atomic_signal_fence(__ATOMIC_SEQ_CST);   // the F loads stay after the flag test
+                stage(I + 1, !a.b_ident && kc_next >= 1, y_staged);
             }
+            const int kmax_next = roww ? (y_staged ? kr : 1) : kc_next;
 
-            if (I < I_last) {   // prefetch the next tile's inputs (consumed after the loop)
+            if (has_next) {   // prefetch the next tile's inputs (consumed after the loop)
                 const int In = I + 1;
                 const int64_t tb = ws_tile_offset(In, J, a.nt);
                 const float* lbp = a.LB + packed_tile_offset(In, In);
@@ -311,6 +363,10 @@ __global__ __launch_bounds__(512) void k_seg(SegArgs a) {
                 const int rn = In * TS + p;
                 pf_s = rn < a.m ? a.scale[rn] : 0.0f;
             }
+
+            float lbr[TS], lar0[TS], lar1[TS];
+#pragma unroll
+            for (int k = 0; k < TS; ++k) { lbr[k] = LBt[p][(k - q0) & 31]; lar0[k] = LAt[q0][(k - p) & 31]; lar1[k] = LAt[q1][(k - p) & 31]; }
 
             // 2. in-tile rounding.  Quantisation without branches: a zero scale
             // gives inv_s = 0, so x = 0, code 0, V = 0 and E = -W~ (the row's
@@ -374,10 +430,15 @@ __global__ __launch_bounds__(512) void k_seg(SegArgs a) {
             // barrier comes once per turn of two rounds.  Buffers alternate
             // with the turn's parity, so a turn never overwrites values that a
             // slower wave may still be reading from the previous turn.
+            // After the barrier of a turn, every wave except the one that is
+            // active in the next turn multiplies one staged pull source of the
+            // next tile (from turn PULL_T0 on, once the direct loads issued
+            // before the loop have landed).
             for (int d0 = 0; d0 < 2 * TS; d0 += TS) {
 #pragma unroll
                 for (int kq = 0; kq < 8; ++kq) {
                     const int tp = kq & 1, kpa = 4 * kq, kpb = 4 * kq + 2;
+                    const int turn = (d0 >> 2) + kq;
                     if (w == kq) {                       // wave-uniform
                         round(kpa, d0 + kpa, tp, 0);
                         __builtin_amdgcn_wave_barrier();
@@ -387,16 +448,27 @@ __global__ __launch_bounds__(512) void k_seg(SegArgs a) {
                     __syncthreads();
                     if (w != kq) update(kpa, tp, 0);
                     update(kpb, tp, 1);
+                    if (turn == PULL_T0 - 1) __builtin_amdgcn_s_waitcnt(0x0F70);   // staged operands landed
+                    if (turn >= PULL_T0 && w != ((kq + 1) & 7) && nk <= kmax_next) {
+                        pull_src(I + 1, nk);
+                        ++nk;
+                    }
                 }
             }
 
-            // 3. publish F (device-coherent), then the flag; E to the ring and X
-            __hip_atomic_store(Yg + p * TS + q0, fo0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            __hip_atomic_store(Yg + p * TS + q1, fo1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            // 3. publish F (device-coherent, whole rows), then the flag; E to the ring and X
+            Fst[p][q0] = fo0;
+            Fst[p][q1] = fo1;
             Xg[q0 * TS + p] = eo0;
             Xg[q1 * TS + p] = eo1;
             Ering[I % RING][q0][p] = eo0;
             Ering[I % RING][q1][p] = eo1;
+            __syncthreads();
+            if (w < 4) {   // wave w stores rows 8w .. 8w + 7, 16 bytes per lane
+                const int r = 8 * w + (l >> 3), c = l & 7;
+                const f32x4 v = *reinterpret_cast<const f32x4*>(&Fst[r][4 * c]);
+                __builtin_amdgcn_raw_buffer_store_b128(v, tile_rsrc(Yg), (r * TS + 4 * c) * 4, 0, CPOL_SC1);
+            }
             __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0): this wave's stores are complete
             __syncthreads();
             if (tid == 0)

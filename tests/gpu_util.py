@@ -2,7 +2,7 @@
 ctypes binding) and compare with the fp64 oracle under the tie-forced
 protocol.
 
-Protocol (spec tolerance): the oracle replays the sequential rounding
+Protocol (the parity tolerance): the oracle replays the sequential rounding
 and, wherever its own pre-rounding value lies within TIE_WINDOW = 1e-4 grid
 steps of a rounding boundary, adopts the GPU's code (both are valid outputs up
 to the tie rule).  Then

@@ -152,7 +152,7 @@ def test_diagonal_hessians_give_round_to_nearest(oracle_mod):
 
 
 def test_fine_grid_returns_W(oracle_mod):
-    """North-star check 3: a grid much finer than W's spread gives V ~ W, with
+    """Corollary 3.4 (no clamping): a grid much finer than W's spread gives V ~ W, with
     |V - W|_max <= (s/2) max_p |L^B_p,:|_1 max_q |L^A_q,:|_1 (V - W0 = L^B E L^A^T)."""
     o = oracle_mod
     p = _rand_problem(24, 20, seed=11, bits=8)
