@@ -522,8 +522,8 @@ struct NodeArgs {
 // v_mfma_f32_32x32x2f32).  Inside a K chunk the 32 k's are split between the
 // two lane halves (half h takes k = 16h + s at step s), so each lane reads 16
 // consecutive floats per operand with four 16-byte LDS loads.  LDS is double
-// buffered and the next chunk is prefetched into registers while the current
-// one is multiplied.  The (source, target) validity masks are separable, so
+// buffered and the chunks two ahead are prefetched into registers while the
+// current one is multiplied.  The (source, target) validity masks are separable, so
 // invalid source tiles are staged as zeros and the sums stay exact.
 //
 // One workgroup per work-list item: the host lists only items with a
@@ -563,21 +563,25 @@ __global__ __launch_bounds__(256, (MT == 4 ? 2 : 4)) void k_node(NodeArgs a) {
         return (I < a.mt && I + kt >= a.K && I + kt < a.Mid) ? a.Y + ws_tile_offset(I, kt, a.nt)
                                                              : nullptr;
     };
-    f32x4 ra[MT], rb[MT];
-    auto load = [&](int kt) {
+    // two register sets: while chunk kt is multiplied from LDS, chunk kt + 1
+    // (loaded one iteration earlier) waits in one set and chunk kt + 2 is in
+    // flight into the other, so each global load has two chunks of MFMA work
+    // to hide behind
+    f32x4 ra[2][MT], rb[2][MT];
+    auto load = [&](int kt, int r) {
 #pragma unroll
         for (int t = 0; t < MT; ++t) {
             const float* pa = a_tile(t, kt);
             const float* pb = b_tile(t, kt);
-            ra[t] = pa ? *reinterpret_cast<const f32x4*>(pa + tid * 4) : f32x4{0.f, 0.f, 0.f, 0.f};
-            rb[t] = pb ? *reinterpret_cast<const f32x4*>(pb + tid * 4) : f32x4{0.f, 0.f, 0.f, 0.f};
+            ra[r][t] = pa ? *reinterpret_cast<const f32x4*>(pa + tid * 4) : f32x4{0.f, 0.f, 0.f, 0.f};
+            rb[r][t] = pb ? *reinterpret_cast<const f32x4*>(pb + tid * 4) : f32x4{0.f, 0.f, 0.f, 0.f};
         }
     };
-    auto store = [&](int s) {
+    auto store = [&](int s, int r) {
 #pragma unroll
         for (int t = 0; t < MT; ++t) {
-            *reinterpret_cast<f32x4*>(&As[s][t * TS + srow][sk]) = ra[t];
-            *reinterpret_cast<f32x4*>(&Bs[s][t * TS + srow][sk]) = rb[t];
+            *reinterpret_cast<f32x4*>(&As[s][t * TS + srow][sk]) = ra[r][t];
+            *reinterpret_cast<f32x4*>(&Bs[s][t * TS + srow][sk]) = rb[r][t];
         }
     };
 
@@ -587,13 +591,10 @@ __global__ __launch_bounds__(256, (MT == 4 ? 2 : 4)) void k_node(NodeArgs a) {
 #pragma unroll
         for (int y = 0; y < WB; ++y) acc[x][y] = f32x16{0};
 
-    load(klo);
-    store(0);
-    __syncthreads();
-    for (int kt = klo; kt < khi; ++kt) {
-        const int s = (kt - klo) & 1;
-        const bool more = kt + 1 < khi;
-        if (more) load(kt + 1);
+    // one K chunk: multiply LDS buffer s; issue the load of chunk kt + 2 into
+    // register set r, then move chunk kt + 1 (set r ^ 1) into buffer s ^ 1
+    auto chunk = [&](int kt, int s, int r) {
+        if (kt + 2 < khi) load(kt + 2, r);
         f32x4 fa[WB][4], fb[WB][4];
 #pragma unroll
         for (int x = 0; x < WB; ++x)
@@ -617,8 +618,19 @@ __global__ __launch_bounds__(256, (MT == 4 ? 2 : 4)) void k_node(NodeArgs a) {
                                                                     fb[y][st >> 2][st & 3],
                                                                     acc[x][y], 0, 0, 0);
         }
-        if (more) store(s ^ 1);
+        if (kt + 1 < khi) store(s ^ 1, r ^ 1);
         __syncthreads();
+    };
+
+    load(klo, 0);
+    if (klo + 1 < khi) load(klo + 1, 1);
+    store(0, 0);
+    __syncthreads();
+    // chunk klo + 2i uses buffer 0 and register set 0 for its prefetch,
+    // chunk klo + 2i + 1 buffer 1 and set 1
+    for (int kt = klo; kt < khi; kt += 2) {
+        chunk(kt, 0, 0);
+        if (kt + 1 < khi) chunk(kt + 1, 1, 1);
     }
 
     // epilogue: block (x, y) of wave (wm, wn) is output solver tile
