@@ -27,6 +27,11 @@ PEAK_FP32_VALU = 157.3      # TFLOP/s, 256 CU x 256 flop/clk x 2.4 GHz (packed d
 PEAK_HBM = 8000.0           # GB/s
 # Paper, Table 3: 4096 x 4096 solved in 0.288 s on one RTX PRO 6000 (fp32).
 PAPER_4096_S = 0.288
+# Paper, Table 3 (seconds on one RTX PRO 6000, fp32): (m, n): (GPTQ, BaKron, BaKron-antidiagonal)
+PAPER_T3 = {(1024, 1024): (0.005, 0.025, 0.092), (2048, 2048): (0.012, 0.074, 0.599),
+            (4096, 4096): (0.025, 0.288, 7.648), (8192, 8192): (0.059, 1.839, 110.379),
+            (8192, 2048): (0.013, 0.335, 6.445), (2048, 8192): (0.046, 0.322, 6.037),
+            (14336, 4096): (0.030, 1.600, 72.886), (4096, 14336): (0.088, 1.717, 73.437)}
 
 
 def log(*a):
@@ -94,6 +99,68 @@ def measured_traffic(kernel: str, workload: str):
     return rec["bytes_per_launch"]
 
 
+def table3(max_antidiag_elems: int):
+    """Runtime comparison on the paper's Table 3 shapes: GPTQ (B = I through
+    the same solver), BaKron and BaKron-antidiagonal (Alg. 3), solve only
+    (factorisation excluded, as in the paper).  Synthetic inputs: A, B the
+    AR(1) Toeplitz matrices rho^|i-j| (rho 0.5 / 0.2), W ~ N(0, 0.02^2), per-row
+    INT4 scales max|W_i|/7, damping 0.01.  Prints one JSON line per shape."""
+    import torch
+    import paper_2608_06291_amd as pk
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream(dev)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+
+    def timed(fn, reps):
+        fn()
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(reps):
+            fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps / 1e3
+
+    def toeplitz(d, rho):
+        i = torch.arange(d, device=dev, dtype=torch.float32)
+        return rho ** (i[:, None] - i[None, :]).abs()
+
+    rows = []
+    for (m, n), paper in PAPER_T3.items():
+        g = torch.Generator(device=dev).manual_seed(m * 100003 + n)
+        W = torch.randn((m, n), generator=g, device=dev) * 0.02
+        s = (W.abs().amax(dim=1) / 7.0).contiguous()
+        A, B = toeplitz(n, 0.5), toeplitz(m, 0.2)
+        f2 = pk.factor(A, B, 0.01)
+        f1 = pk.factor(A, None, 0.01)
+        codes = torch.empty((m, n), dtype=torch.int8, device=dev)
+        V = torch.empty((m, n), dtype=torch.float32, device=dev)
+        t_gptq = timed(lambda: pk.solve(W, f1, 4, s, codes=codes, V=V), 10)
+        t_bk = timed(lambda: pk.solve(W, f2, 4, s, codes=codes, V=V), 10)
+        t_ad = None
+        if m * n <= max_antidiag_elems:
+            t0 = time.perf_counter()
+            pk.solve_antidiag(W, f2, 4, s, codes=codes, V=V)
+            torch.cuda.synchronize()
+            t_ad = time.perf_counter() - t0
+        f1.close()
+        f2.close()
+        r = dict(m=m, n=n, gptq_s=t_gptq, bakron_s=t_bk, antidiag_s=t_ad,
+                 speedup=(t_ad / t_bk) if t_ad else None,
+                 paper_s=dict(gptq=paper[0], bakron=paper[1], antidiag=paper[2],
+                              speedup=paper[2] / paper[1]))
+        rows.append(r)
+        print(json.dumps(r), flush=True)
+        del W, A, B, codes, V
+        torch.cuda.empty_cache()
+    log("| m x n | GPTQ (s) | BaKron (s) | BaKron-antidiag (s) | speedup | paper speedup |")
+    for r in rows:
+        ad = f"{r['antidiag_s']:.3f}" if r["antidiag_s"] else "-"
+        sp = f"{r['speedup']:.1f}x" if r["speedup"] else "-"
+        log(f"| {r['m']} x {r['n']} | {r['gptq_s']:.4f} | {r['bakron_s']:.4f} | {ad} | {sp} | "
+            f"{r['paper_s']['speedup']:.1f}x |")
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -107,6 +174,11 @@ def main():
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="only run a plain device-to-device copy of this many MiB (10 times) and "
                          "exit: the reference for scaling rocprofv3 FETCH_SIZE/WRITE_SIZE counters")
+    ap.add_argument("--table3", action="store_true",
+                    help="only run the runtime comparison on the paper's Table 3 shapes (GPTQ, BaKron, "
+                         "BaKron-antidiagonal) and exit; one JSON line per shape")
+    ap.add_argument("--table3-max-antidiag-elems", type=int, default=1 << 27,
+                    help="skip BaKron-antidiagonal (quartic work) above this many matrix entries")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: --gpus {args.gpus} is not supported: the BaKron solve runs on one "
@@ -116,6 +188,10 @@ def main():
 
     import numpy as np
     import torch
+
+    if args.table3:
+        table3(args.table3_max_antidiag_elems)
+        return
 
     if args.copy_calibration_mib > 0:
         nbytes = args.copy_calibration_mib << 20

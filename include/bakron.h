@@ -108,6 +108,26 @@ bakron_status bakron_solve_debug(const float *W, int64_t m, int64_t n, const bak
                                  bakron_quantizer q, int8_t *codes, float *V, float *pre,
                                  hipStream_t stream);
 
+/*
+ * bakron_solve_antidiag -- the same rounding by BaKron-antidiagonal (Alg. 3):
+ * element anti-diagonal after element anti-diagonal, each rounded in
+ * parallel and followed by the full update W~ += L^B * antidiag_k(E) * L^A^T.
+ * Thm 3.2: the output equals bakron_solve's (up to fp32 summation order, i.e.
+ * possibly different codes at entries within rounding noise of a boundary).
+ * Its total work is O(m^2 n^2) against BaKron's O(mn(m+n)) (Table 1); it is
+ * the reference point of the paper's runtime comparison (Table 3) and is
+ * provided for that comparison, not as a production path.
+ *
+ * Arguments, layouts, ownership and errors as bakron_solve; pre may be NULL
+ * (else as bakron_solve_debug).  Adds m + n - 1 pairs of launches on
+ * `stream`.  Workspace: 4 * (m * n + 32 * ceil(m / 32)) bytes, allocated on the first
+ * call for a shape and kept on the handle (separate from bakron_solve's).
+ * Dimensions above 2^30 -> BAKRON_EINVAL.
+ */
+bakron_status bakron_solve_antidiag(const float *W, int64_t m, int64_t n, const bakron_factors *f,
+                                    bakron_quantizer q, int8_t *codes, float *V, float *pre,
+                                    hipStream_t stream);
+
 /* Frees the handle, its factors and its workspace (synchronises the device
  * work that used them).  NULL is a no-op. */
 void bakron_factors_free(bakron_factors *f);

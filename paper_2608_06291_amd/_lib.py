@@ -17,7 +17,7 @@ BAKRON_OK, BAKRON_EINVAL, BAKRON_ENOTSPD, BAKRON_ENOMEM, BAKRON_EHIP = range(5)
 EXPORTED = ("bakron_factor", "bakron_solve", "bakron_solve_debug", "bakron_factors_free",
             "bakron_status_string", "bakron_factors_error", "bakron_last_error",
             "bakron_factor_export", "bakron_profile_enable", "bakron_profile_read",
-            "bakron_solve_check")
+            "bakron_solve_check", "bakron_solve_antidiag")
 
 _lib = None
 
@@ -72,6 +72,9 @@ def load(path: str = LIB_PATH):
     lib.bakron_profile_enable.argtypes = [vp, ctypes.c_int]
     lib.bakron_profile_read.restype = ctypes.c_int
     lib.bakron_profile_read.argtypes = [vp, ctypes.POINTER(KernelStat), ctypes.c_int]
+    lib.bakron_solve_antidiag.restype = ctypes.c_int
+    lib.bakron_solve_antidiag.argtypes = [vp, ctypes.c_int64, ctypes.c_int64, vp, _Quantizer, vp, vp,
+                                          vp, vp]
     lib.bakron_solve_check.restype = ctypes.c_int
     lib.bakron_solve_check.argtypes = [vp, vp, ctypes.POINTER(ctypes.c_int32)]
     _lib = lib
@@ -219,3 +222,33 @@ def solve(W, f: Factors, bits: int, scale, codes=None, V=None, pre=None, debug: 
     if st != BAKRON_OK:
         raise BakronError(st, f.error())
     return (codes, V, pre) if debug else (codes, V)
+
+
+def solve_antidiag(W, f: Factors, bits: int, scale, codes=None, V=None, pre=None):
+    """bakron_solve_antidiag (BaKron-antidiagonal, Alg. 3) on the current stream.
+
+    Returns (codes int8, V fp32), or (codes, V, pre) when a pre buffer is given.
+    """
+    import torch
+    lib = load()
+    _check_dev(W, "W", torch.float32)
+    _check_dev(scale, "scale", torch.float32)
+    m, n = W.shape
+    if scale.numel() != m:
+        raise ValueError("scale must have m entries")
+    if codes is None:
+        codes = torch.empty((m, n), dtype=torch.int8, device=W.device)
+    if V is None:
+        V = torch.empty((m, n), dtype=torch.float32, device=W.device)
+    _check_dev(codes, "codes", torch.int8)
+    _check_dev(V, "V", torch.float32)
+    if pre is not None:
+        _check_dev(pre, "pre", torch.float32)
+    q = _Quantizer(int(bits), ctypes.c_void_p(scale.data_ptr()).value)
+    st = lib.bakron_solve_antidiag(ctypes.c_void_p(W.data_ptr()), m, n, f.handle, q,
+                                   ctypes.c_void_p(codes.data_ptr()), ctypes.c_void_p(V.data_ptr()),
+                                   ctypes.c_void_p(pre.data_ptr() if pre is not None else None),
+                                   _stream(torch, W.device))
+    if st != BAKRON_OK:
+        raise BakronError(st, f.error())
+    return (codes, V) if pre is None else (codes, V, pre)

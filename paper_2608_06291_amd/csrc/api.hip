@@ -24,6 +24,9 @@ hipError_t run_plan(hipStream_t st, const Plan& plan, const float* W, int64_t m,
                     const float* scale, float qmax, int8_t* codes, float* V, float* pre, int knear,
                     const int4* items, hipEvent_t* tim);
 int plan_timed_launches(const Plan& plan);
+hipError_t run_antidiag(hipStream_t st, const float* W, int64_t m, int64_t n, float* Wt,
+                        float* delta, const float* LA, const float* LB, const float* scale,
+                        float qmax, int8_t* codes, float* V, float* pre);
 }  // namespace bk
 
 struct bakron_factors {
@@ -48,6 +51,9 @@ struct bakron_factors {
     std::vector<hipEvent_t> tim;
     std::vector<int> tclass;        // 0 prep, 1 segment, 2 node
     std::vector<double> tflops, tmfma;
+    // BaKron-antidiagonal working copy of W and one diagonal's errors
+    int64_t ad_m = -1, ad_n = -1;
+    float* ad_mem = nullptr;
     std::string err;
 };
 
@@ -307,14 +313,29 @@ extern "C" void bakron_factors_free(bakron_factors* f) {
     if (f->LA) hipFree(f->LA);
     if (f->LB) hipFree(f->LB);
     if (f->ws_mem) hipFree(f->ws_mem);
+    if (f->ad_mem) hipFree(f->ad_mem);
     if (f->items) hipFree(f->items);
     for (hipEvent_t ev : f->tim) hipEventDestroy(ev);
     if (cur != f->device) hipSetDevice(cur);
     delete f;
 }
 
+// B = I: the packed identity factor grows to the requested m
+static bakron_status ensure_identity(bakron_factors* f, int64_t mt) {
+    if (!f->b_ident || f->LB_tiles >= mt) return BAKRON_OK;
+    if (f->LB) hipFree(f->LB);
+    f->LB = nullptr;
+    hipError_t e = hipMalloc(&f->LB, sizeof(float) * (size_t)(mt * (mt + 1) / 2) * bk::TILE_ELEMS);
+    if (e == hipSuccess) e = bk::pack_identity(0, mt, f->LB);
+    if (e == hipSuccess) e = hipDeviceSynchronize();
+    if (e != hipSuccess) return hip_fail(&f->err, e, "bakron_solve: identity factor");
+    f->LB_tiles = mt;
+    return BAKRON_OK;
+}
+
 static bakron_status ensure_workspace(bakron_factors* f, int64_t m, int64_t n) {
     if (f->ws_m == m && f->ws_n == n && f->ws_mem) return BAKRON_OK;
+    bakron_status st;
     const int64_t mt = cdiv(m, bk::TS), nt = cdiv(n, bk::TS);
     if (f->ws_mem) { hipFree(f->ws_mem); f->ws_mem = nullptr; }
     f->ws_m = f->ws_n = -1;
@@ -328,16 +349,8 @@ static bakron_status ensure_workspace(bakron_factors* f, int64_t m, int64_t n) {
     int* ints = reinterpret_cast<int*>(base + 2 * fbytes);
     f->ws = bk::Workspace{reinterpret_cast<float*>(base), reinterpret_cast<float*>(base + fbytes),
                           ints, ints + tiles, ints + tiles + f->plan.nseg};
-    // identity B grows to the requested m
-    if (f->b_ident && f->LB_tiles < mt) {
-        if (f->LB) hipFree(f->LB);
-        f->LB = nullptr;
-        e = hipMalloc(&f->LB, sizeof(float) * (size_t)(mt * (mt + 1) / 2) * bk::TILE_ELEMS);
-        if (e == hipSuccess) e = bk::pack_identity(0, mt, f->LB);
-        if (e == hipSuccess) e = hipDeviceSynchronize();
-        if (e != hipSuccess) return hip_fail(&f->err, e, "bakron_solve: identity factor");
-        f->LB_tiles = mt;
-    }
+    st = ensure_identity(f, mt);
+    if (st != BAKRON_OK) return st;
     if (f->items) { hipFree(f->items); f->items = nullptr; }
     if (!f->items_host.empty()) {
         const size_t ib = sizeof(int4) * f->items_host.size();
@@ -359,29 +372,38 @@ static bakron_status ensure_workspace(bakron_factors* f, int64_t m, int64_t n) {
     return BAKRON_OK;
 }
 
+// argument checks shared by the solve entry points (host side, synchronous)
+static bakron_status check_solve_args(bakron_factors* f, const char* who, const float* W, int64_t m,
+                                      int64_t n, bakron_quantizer q, const int8_t* codes,
+                                      const float* V) {
+    if (!W || !codes || !V || !q.scale || m <= 0 || n <= 0) {
+        f->err = std::string(who) + ": null pointer or non-positive size";
+        return BAKRON_EINVAL;
+    }
+    if (n != f->n || (!f->b_ident && m != f->m)) {
+        f->err = std::string(who) + ": (m, n) does not match the factor handle";
+        return BAKRON_EINVAL;
+    }
+    if (q.bits < 2 || q.bits > 8) {
+        f->err = std::string(who) + ": bits must be in [2, 8]";
+        return BAKRON_EINVAL;
+    }
+    if ((m + bk::TS) * (n + bk::TS) > ((int64_t)1 << 40)) {
+        f->err = std::string(who) + ": matrix too large";
+        return BAKRON_EINVAL;
+    }
+    return BAKRON_OK;
+}
+
 static bakron_status solve_impl(const float* W, int64_t m, int64_t n, const bakron_factors* fc,
                                 bakron_quantizer q, int8_t* codes, float* V, float* pre,
                                 hipStream_t stream) {
     bakron_factors* f = const_cast<bakron_factors*>(fc);
     if (!f) return BAKRON_EINVAL;
     f->err.clear();
-    if (!W || !codes || !V || !q.scale || m <= 0 || n <= 0) {
-        f->err = "bakron_solve: null pointer or non-positive size";
-        return BAKRON_EINVAL;
-    }
-    if (n != f->n || (!f->b_ident && m != f->m)) {
-        f->err = "bakron_solve: (m, n) does not match the factor handle";
-        return BAKRON_EINVAL;
-    }
-    if (q.bits < 2 || q.bits > 8) {
-        f->err = "bakron_solve: bits must be in [2, 8]";
-        return BAKRON_EINVAL;
-    }
-    if ((m + bk::TS) * (n + bk::TS) > ((int64_t)1 << 40)) {
-        f->err = "bakron_solve: matrix too large";
-        return BAKRON_EINVAL;
-    }
-    bakron_status st = ensure_workspace(f, m, n);
+    bakron_status st = check_solve_args(f, "bakron_solve", W, m, n, q, codes, V);
+    if (st != BAKRON_OK) return st;
+    st = ensure_workspace(f, m, n);
     if (st != BAKRON_OK) return st;
     const int mt = (int)cdiv(m, bk::TS), nt = (int)cdiv(n, bk::TS);
     const float qmax = (float)((1 << (q.bits - 1)) - 1);
@@ -419,6 +441,37 @@ extern "C" bakron_status bakron_solve_debug(const float* W, int64_t m, int64_t n
         return BAKRON_EINVAL;
     }
     return solve_impl(W, m, n, f, q, codes, V, pre, stream);
+}
+
+extern "C" bakron_status bakron_solve_antidiag(const float* W, int64_t m, int64_t n,
+                                             const bakron_factors* fc, bakron_quantizer q,
+                                             int8_t* codes, float* V, float* pre,
+                                             hipStream_t stream) {
+    bakron_factors* f = const_cast<bakron_factors*>(fc);
+    if (!f) return BAKRON_EINVAL;
+    f->err.clear();
+    bakron_status st = check_solve_args(f, "bakron_solve_antidiag", W, m, n, q, codes, V);
+    if (st != BAKRON_OK) return st;
+    if (m > (int64_t)1 << 30 || n > (int64_t)1 << 30) {
+        f->err = "bakron_solve_antidiag: dimension too large";
+        return BAKRON_EINVAL;
+    }
+    st = ensure_identity(f, cdiv(m, bk::TS));
+    if (st != BAKRON_OK) return st;
+    if (f->ad_m != m || f->ad_n != n || !f->ad_mem) {
+        if (f->ad_mem) { hipFree(f->ad_mem); f->ad_mem = nullptr; }
+        f->ad_m = f->ad_n = -1;
+        const size_t elems = (size_t)cdiv(m * n, 64) * 64 + (size_t)(cdiv(m, bk::TS) * bk::TS);
+        hipError_t e = hipMalloc(&f->ad_mem, sizeof(float) * elems);
+        if (e != hipSuccess) return hip_fail(&f->err, e, "bakron_solve_antidiag: hipMalloc (workspace)");
+        f->ad_m = m;
+        f->ad_n = n;
+    }
+    const float qmax = (float)((1 << (q.bits - 1)) - 1);
+    hipError_t e = bk::run_antidiag(stream, W, m, n, f->ad_mem, f->ad_mem + (size_t)cdiv(m * n, 64) * 64, f->LA,
+                                    f->LB, q.scale, qmax, codes, V, pre);
+    if (e != hipSuccess) return hip_fail(&f->err, e, "bakron_solve_antidiag: launch");
+    return BAKRON_OK;
 }
 
 extern "C" bakron_status bakron_factor_export(const bakron_factors* f, int which, float* dst,

@@ -112,3 +112,23 @@ def check_against_oracle(p, codes, V, pre, oracle, label=""):
         free = oracle.solve(p["W"], p["A"], p["B"], p["damp"], p["scale"], p["bits"])
         assert np.array_equal(free["codes"], codes), f"{label}: free-running mismatch"
     return res
+
+
+def gpu_run_antidiag(p):
+    """Factor + BaKron-antidiagonal solve on cuda:0; returns numpy codes, V, pre."""
+    import torch
+    import paper_2608_06291_amd as pk
+    dev = torch.device("cuda:0")
+    A = torch.from_numpy(np.ascontiguousarray(p["A"], np.float32)).to(dev)
+    B = None if p["B"] is None else torch.from_numpy(np.ascontiguousarray(p["B"], np.float32)).to(dev)
+    W = torch.from_numpy(np.ascontiguousarray(p["W"], np.float32)).to(dev)
+    s = torch.from_numpy(np.ascontiguousarray(p["scale"], np.float32)).to(dev)
+    f = pk.factor(A, B, p["damp"])
+    codes = torch.full(W.shape, 100, dtype=torch.int8, device=dev)
+    V = torch.full(W.shape, float("nan"), dtype=torch.float32, device=dev)
+    pre = torch.full(W.shape, float("nan"), dtype=torch.float32, device=dev)
+    pk.solve_antidiag(W, f, p["bits"], s, codes=codes, V=V, pre=pre)
+    torch.cuda.synchronize()
+    out = (codes.cpu().numpy(), V.cpu().numpy(), pre.cpu().numpy())
+    f.close()
+    return out
