@@ -90,10 +90,18 @@ bakron_status bakron_factor(const float *A, int64_t n, const float *B, int64_t m
  *   V      device, m x n fp32 output, V_ij = s_i * codes_ij (one fp32 product)
  *
  * The first call for a given (m, n) allocates the workspace (about 8*m*n
- * bytes plus one int per 32 x 32 tile) and builds the launch plan; later
+ * bytes plus one int per 32 x 32 tile) and builds the launch plans; later
  * calls with the same (m, n) allocate nothing and never synchronise the host.
- * All work is enqueued on `stream`.  Kernel faults surface as BAKRON_EHIP on
- * a later call or at the caller's synchronisation.
+ * The work is ordered after everything enqueued on `stream` before the call,
+ * and everything enqueued on `stream` after it is ordered after the solve.
+ * On a stream other than the legacy default stream (0 / hipStreamLegacy) the
+ * solve may fork onto two streams of the handle, restricted to disjoint CU
+ * sets (the divide-and-conquer pushes into later segments overlap with the
+ * segment launches), and joins back into `stream` with events; on the legacy
+ * default stream, which synchronises implicitly with such streams, and with
+ * the environment variable BAKRON_DEFER=0, everything runs on `stream`.  The
+ * results are bitwise the same either way.  Kernel faults surface as
+ * BAKRON_EHIP on a later call or at the caller's synchronisation.
  */
 bakron_status bakron_solve(const float *W, int64_t m, int64_t n, const bakron_factors *f,
                            bakron_quantizer q, int8_t *codes, float *V, hipStream_t stream);

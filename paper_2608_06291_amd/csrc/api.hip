@@ -19,10 +19,11 @@ hipError_t factor_one(hipStream_t s, const float* X, int64_t d, double lam, doub
 hipError_t pack_identity(hipStream_t s, int64_t nt, float* packed);
 hipError_t unpack_factor(hipStream_t s, const float* packed, int64_t d, float* dst);
 
-hipError_t run_plan(hipStream_t st, const Plan& plan, const float* W, int64_t m, int64_t n, int mt,
-                    int nt, const Workspace& ws, const float* LA, const float* LB, int b_ident,
-                    const float* scale, float qmax, int8_t* codes, float* V, float* pre, int knear,
-                    const int4* items, hipEvent_t* tim);
+hipError_t run_plan(hipStream_t st, hipStream_t side, const Plan& plan, const float* W, int64_t m,
+                    int64_t n, int mt, int nt, const Workspace& ws, const float* LA, const float* LB,
+                    int b_ident, const float* scale, float qmax, int8_t* codes, float* V, float* pre,
+                    int knear, const int4* items, hipEvent_t* tim, hipEvent_t* ev_rel,
+                    hipEvent_t* ev_side);
 int plan_timed_launches(const Plan& plan);
 hipError_t run_antidiag(hipStream_t st, const float* W, int64_t m, int64_t n, float* Wt,
                         float* delta, const float* LA, const float* LB, const float* scale,
@@ -42,15 +43,26 @@ struct bakron_factors {
     void* ws_mem = nullptr;         // X, Y tile arrays, flags, counters, status (bk::Workspace)
     bk::Workspace ws{};
     int knear = 8;
-    bk::Plan plan;
-    std::vector<int4> items_host;   // node work lists of the plan
+    // plan[0]: everything on the caller's stream; plan[1]: with side ops
+    // (empty if the side stream is not used).  Both make the same additions
+    // to every tile in the same order, so their results are identical.
+    bk::Plan plan[2];
+    int last_plan = 0;
+    std::vector<int4> items_host;   // node work lists of both plans
     int4* items = nullptr;
     // measurement hook: per timed launch (enqueue order) its class and work
     int prof = 0;
     int prof_valid = 0;
     std::vector<hipEvent_t> tim;
-    std::vector<int> tclass;        // 0 prep, 1 segment, 2 node
-    std::vector<double> tflops, tmfma;
+    std::vector<int> tclass[2];     // per plan: 0 prep, 1 segment, 2 node
+    std::vector<double> tflops[2], tmfma[2];
+    // with deferred node pushes: the side stream (CUs [side_cu_lo, #CUs)) and
+    // the stream that carries the main ops (the other CUs); both forked from
+    // and joined back into the caller's stream (null if not used yet)
+    hipStream_t side = nullptr, main = nullptr;
+    int side_cu_lo = -1;
+    std::vector<hipEvent_t> ev_rel, ev_side;
+    hipEvent_t ev_fork = nullptr, ev_join = nullptr;
     // BaKron-antidiagonal working copy of W and one diagonal's errors
     int64_t ad_m = -1, ad_n = -1;
     float* ad_mem = nullptr;
@@ -91,9 +103,10 @@ static inline int imin(int a, int b) { return a < b ? a : b; }
 
 // Algorithmic flops of one node launch: 2*TS^3 per (source, target) tile
 // pair it pushes, mirroring the kernel's source ranges and masks.
-static double node_alg_flops(int K, int Mid, int L, int mt, int nt, int knear, int b_ident) {
+static double node_alg_flops(int K, int Mid, int tlo, int thi, int mt, int nt, int knear,
+                             int b_ident) {
     double f = 0.0;
-    for (int D = Mid; D < L; ++D) {
+    for (int D = tlo; D < thi; ++D) {
         for (int I = imax(0, D - (nt - 1)); I <= imin(D, mt - 1); ++I) {
             const int J = D - I;
             if (!b_ident) f += imax(0, imin(Mid - J, I - knear) - imax(K - J, 0));
@@ -103,25 +116,27 @@ static double node_alg_flops(int K, int Mid, int L, int mt, int nt, int knear, i
     return f * 2.0 * bk::TS * bk::TS * bk::TS;
 }
 
-// Work list of one node for MT x MT macro tiles: every (macro tile, push
-// kind) with at least one target tile in [Mid, L) and a non-empty source
-// range, longest source range first.
-static void node_items(int K, int Mid, int L, int mt, int nt, int knear, int b_ident, int MT,
-                       std::vector<int4>& out) {
+// Work list of a push from sources on [K, Mid) into targets on [tlo, thi)
+// for MT x MT macro tiles: every (macro tile, push kind) with at least one
+// target tile in [tlo, thi) and a non-empty source range, longest source
+// range first.  A macro tile's source range depends only on its position, so
+// a target tile receives the same sum whichever target range lists it.
+static void node_items(int K, int Mid, int tlo, int thi, int mt, int nt, int knear, int b_ident,
+                       int MT, std::vector<int4>& out) {
     out.clear();
     const int nmi = (mt + MT - 1) / MT, nmj = (nt + MT - 1) / MT;
     for (int mi = 0; mi < nmi; ++mi) {
         const int I0 = mi * MT;
-        // macro columns whose tile anti-diagonals can meet [Mid, L)
-        const int mj_lo = imax(0, (Mid - 2 * (MT - 1) - I0 + MT - 1) / MT - 1);
+        // macro columns whose tile anti-diagonals can meet [tlo, thi)
+        const int mj_lo = imax(0, (tlo - 2 * (MT - 1) - I0 + MT - 1) / MT - 1);
         for (int mj = mj_lo; mj < nmj; ++mj) {
             const int J0 = mj * MT;
-            if (I0 + J0 >= L) break;
+            if (I0 + J0 >= thi) break;
             bool target = false;
             for (int a = 0; a < MT && !target; ++a)
                 for (int b = 0; b < MT && !target; ++b) {
                     const int I = I0 + a, J = J0 + b;
-                    target = I < mt && J < nt && I + J >= Mid && I + J < L;
+                    target = I < mt && J < nt && I + J >= tlo && I + J < thi;
                 }
             if (!target) continue;
             if (!b_ident) {
@@ -146,9 +161,52 @@ static inline int diag_hi(int D, int mt) { return imin(D, mt - 1); }
 // anti-diagonals becomes one persistent segment launch (all its pairs are at
 // distance <= knear and are pulled by their targets); a wider one recurses on
 // [K, Mid), pushes S1 -> S2 for pairs farther apart than knear, then recurses
-// on [Mid, L).  Split at floor((K+L)/2) (App. C: balanced splits).
-static void build_ops(int K, int L, int mt, int nt, int knear, int b_ident, bk::Plan& plan,
-                      std::vector<int4>& items) {
+// on [Mid, L).  Split at floor((K+L)/2) (App. C: balanced splits).  With
+// `defer`, a node's push is cut by the segments of its right subtree: the
+// part into the first one is a main op, the others are side ops released
+// after the left subtree (they may run while the segments before their
+// targets are solved).
+static void leaves(int K, int L, int knear, std::vector<std::pair<int, int>>& out) {
+    if (L - K <= knear + 1) {
+        out.push_back({K, L});
+        return;
+    }
+    const int Mid = (K + L) / 2;
+    leaves(K, Mid, knear, out);
+    leaves(Mid, L, knear, out);
+}
+
+static bool node_op(int K, int Mid, int tlo, int thi, int mt, int nt, int knear, int b_ident,
+                    std::vector<int4>& items, bk::PlanOp& op) {
+    const double T = bk::TS;
+    int MT = bk::MACRO;
+    std::vector<int4> its;
+    node_items(K, Mid, tlo, thi, mt, nt, knear, b_ident, 4, its);
+    if ((int)its.size() < 512) {
+        MT = 2;
+        node_items(K, Mid, tlo, thi, mt, nt, knear, b_ident, 2, its);
+    }
+    if (its.empty()) return false;
+    op = bk::PlanOp{};
+    op.kind = 1;
+    op.K = K;
+    op.Mid = Mid;
+    op.L = thi;
+    op.tlo = tlo;
+    op.thi = thi;
+    op.macro = MT;
+    op.item_off = (int)items.size();
+    op.item_cnt = (int)its.size();
+    op.rel = -1;
+    const double chunkf = 2.0 * (MT * T) * (MT * T) * T;
+    for (const int4& it : its) op.mfma_flops += (it.w - (it.z >> 1)) * chunkf;
+    op.flops = node_alg_flops(K, Mid, tlo, thi, mt, nt, knear, b_ident);
+    items.insert(items.end(), its.begin(), its.end());
+    return true;
+}
+
+static void build_ops(int K, int L, int mt, int nt, int knear, int b_ident, bool defer,
+                      bk::Plan& plan, std::vector<int4>& items) {
     const double T = bk::TS, pair = 2.0 * T * T * T;
     if (L - K <= knear + 1) {
         bk::PlanOp op{};
@@ -165,6 +223,9 @@ static void build_ops(int K, int L, int mt, int nt, int knear, int b_ident, bk::
                 pulls += imin(J, knear);
             }
         op.Mid = K;
+        op.tlo = K;
+        op.thi = L;
+        op.rel = -1;
         op.strip_lo = imax(0, K - (mt - 1));
         op.nstrips = imin(nt - 1, L - 1) - op.strip_lo + 1;
         op.counter = plan.nseg++;
@@ -174,38 +235,55 @@ static void build_ops(int K, int L, int mt, int nt, int knear, int b_ident, bk::
         return;
     }
     const int Mid = (K + L) / 2;
-    build_ops(K, Mid, mt, nt, knear, b_ident, plan, items);
-    int MT = bk::MACRO;
-    std::vector<int4> its;
-    node_items(K, Mid, L, mt, nt, knear, b_ident, 4, its);
-    if ((int)its.size() < 512) {
-        MT = 2;
-        node_items(K, Mid, L, mt, nt, knear, b_ident, 2, its);
-    }
-    if (!its.empty()) {
-        bk::PlanOp op{};
-        op.kind = 1;
-        op.K = K;
-        op.Mid = Mid;
-        op.L = L;
-        op.macro = MT;
-        op.item_off = (int)items.size();
-        op.item_cnt = (int)its.size();
-        const double chunkf = 2.0 * (MT * T) * (MT * T) * T;
-        for (const int4& it : its) op.mfma_flops += (it.w - (it.z >> 1)) * chunkf;
-        op.flops = node_alg_flops(K, Mid, L, mt, nt, knear, b_ident);
-        items.insert(items.end(), its.begin(), its.end());
+    build_ops(K, Mid, mt, nt, knear, b_ident, defer, plan, items);
+    // With `defer`, the push into the first right segment is a main op and the
+    // pushes into the later segments are side ops released after the left
+    // subtree; every target tile receives one addition per node either way.
+    const int rel = (int)plan.ops.size() - 1;
+    std::vector<std::pair<int, int>> right;
+    leaves(Mid, L, knear, right);
+    bk::PlanOp op;
+    if (node_op(K, Mid, Mid, defer ? right[0].second : L, mt, nt, knear, b_ident, items, op))
         plan.ops.push_back(op);
-    }
-    build_ops(Mid, L, mt, nt, knear, b_ident, plan, items);
+    if (defer)
+        for (size_t j = 1; j < right.size(); ++j)
+            if (node_op(K, Mid, right[j].first, right[j].second, mt, nt, knear, b_ident, items, op)) {
+                op.rel = rel;
+                plan.side.push_back(op);
+            }
+    build_ops(Mid, L, mt, nt, knear, b_ident, defer, plan, items);
 }
 
-static void build_plan(int mt, int nt, int knear, int b_ident, bk::Plan& plan,
+// side ops in deadline order (target segment, then release); per main op the
+// number of side ops that must be complete before it (those whose targets
+// start at or before its own); the host enqueue order
+static void finish_plan(bk::Plan& plan) {
+    std::stable_sort(plan.side.begin(), plan.side.end(), [](const bk::PlanOp& a, const bk::PlanOp& b) {
+        return a.tlo != b.tlo ? a.tlo < b.tlo : a.rel < b.rel;
+    });
+    for (bk::PlanOp& op : plan.ops) op.rec_rel = 0;
+    for (const bk::PlanOp& so : plan.side) plan.ops[so.rel].rec_rel = 1;
+    size_t c = 0;
+    for (bk::PlanOp& op : plan.ops) {
+        while (c < plan.side.size() && plan.side[c].tlo <= op.tlo) ++c;
+        op.need_side = (int)c;
+    }
+    plan.order.clear();
+    size_t ps = 0;
+    for (size_t i = 0; i < plan.ops.size(); ++i) {
+        plan.order.push_back({0, (int)i});
+        while (ps < plan.side.size() && plan.side[ps].rel <= (int)i) plan.order.push_back({1, (int)ps++});
+    }
+}
+
+static void build_plan(int mt, int nt, int knear, int b_ident, bool defer, bk::Plan& plan,
                        std::vector<int4>& items) {
     plan.ops.clear();
+    plan.side.clear();
     plan.nseg = 0;
     items.clear();
-    build_ops(0, mt + nt - 1, mt, nt, knear, b_ident, plan, items);
+    build_ops(0, mt + nt - 1, mt, nt, knear, b_ident, defer, plan, items);
+    finish_plan(plan);
 }
 
 extern "C" bakron_status bakron_factor(const float* A, int64_t n, const float* B, int64_t m,
@@ -314,6 +392,12 @@ extern "C" void bakron_factors_free(bakron_factors* f) {
     if (f->LB) hipFree(f->LB);
     if (f->ws_mem) hipFree(f->ws_mem);
     if (f->ad_mem) hipFree(f->ad_mem);
+    if (f->side) hipStreamDestroy(f->side);
+    if (f->main) hipStreamDestroy(f->main);
+    if (f->ev_fork) hipEventDestroy(f->ev_fork);
+    if (f->ev_join) hipEventDestroy(f->ev_join);
+    for (hipEvent_t ev : f->ev_rel) hipEventDestroy(ev);
+    for (hipEvent_t ev : f->ev_side) hipEventDestroy(ev);
     if (f->items) hipFree(f->items);
     for (hipEvent_t ev : f->tim) hipEventDestroy(ev);
     if (cur != f->device) hipSetDevice(cur);
@@ -333,22 +417,99 @@ static bakron_status ensure_identity(bakron_factors* f, int64_t mt) {
     return BAKRON_OK;
 }
 
+// The plan of an mt x nt tile grid.  Node pushes into later segments go to a
+// side stream restricted to the CUs that no segment launch needs (a segment
+// has one persistent workgroup per strip, at most one per CU): CUs
+// [R, #CUs) with R = max(#CUs / 2, widest segment rounded up to 32), when at
+// least 64 CUs remain.  BAKRON_DEFER=0 keeps every push on the caller's
+// stream, and so does a failure to create the side stream.
+static bakron_status plan_with_side_stream(bakron_factors* f, int mt, int nt) {
+    build_plan(mt, nt, f->knear, f->b_ident, false, f->plan[0], f->items_host);
+    f->plan[1] = bk::Plan{};
+    const char* env = std::getenv("BAKRON_DEFER");
+    if (env && std::atoi(env) == 0) return BAKRON_OK;
+    hipDeviceProp_t prop;
+    if (hipGetDeviceProperties(&prop, f->device) != hipSuccess) return BAKRON_OK;
+    const int ncu = prop.multiProcessorCount;
+    int widest = 0;
+    for (const bk::PlanOp& op : f->plan[0].ops)
+        if (op.kind == 0) widest = imax(widest, op.nstrips);
+    const int R = imax(ncu / 2, (widest + 31) / 32 * 32);
+    if (ncu - R < 64) return BAKRON_OK;
+    if (!f->side || f->side_cu_lo != R) {
+        for (hipStream_t* ps : {&f->side, &f->main})
+            if (*ps) {
+                (void)hipStreamSynchronize(*ps);
+                (void)hipStreamDestroy(*ps);
+                *ps = nullptr;
+            }
+        f->side_cu_lo = -1;
+        // main ops on CUs [0, R), side ops on [R, #CUs): a persistent segment
+        // workgroup never sits on a CU a side push waits for, and the reverse
+        auto masked = [&](int lo, int hi, hipStream_t* out) {
+            std::vector<uint32_t> mask((size_t)(ncu + 31) / 32, 0u);
+            for (int c = lo; c < hi; ++c) mask[(size_t)c / 32] |= 1u << (c % 32);
+            if (hipExtStreamCreateWithCUMask(out, (uint32_t)mask.size(), mask.data()) != hipSuccess ||
+                !*out) {
+                *out = nullptr;
+                (void)hipGetLastError();
+                return false;
+            }
+            return true;
+        };
+        if (!masked(0, R, &f->main) || !masked(R, ncu, &f->side)) {
+            if (f->main) { (void)hipStreamDestroy(f->main); f->main = nullptr; }
+            return BAKRON_OK;   // no side stream: every push stays on the caller's stream
+        }
+        f->side_cu_lo = R;
+    }
+    auto grow = [](std::vector<hipEvent_t>& v, size_t need) {
+        while (v.size() < need) {
+            hipEvent_t ev;
+            if (hipEventCreateWithFlags(&ev, hipEventDisableTiming) != hipSuccess) return false;
+            v.push_back(ev);
+        }
+        return true;
+    };
+    if ((!f->ev_fork && hipEventCreateWithFlags(&f->ev_fork, hipEventDisableTiming) != hipSuccess) ||
+        (!f->ev_join && hipEventCreateWithFlags(&f->ev_join, hipEventDisableTiming) != hipSuccess)) {
+        (void)hipGetLastError();
+        return BAKRON_OK;
+    }
+    bk::Plan deferred;
+    std::vector<int4> items;
+    build_plan(mt, nt, f->knear, f->b_ident, true, deferred, items);
+    if (!grow(f->ev_rel, deferred.ops.size()) || !grow(f->ev_side, deferred.side.size())) {
+        (void)hipGetLastError();
+        return BAKRON_OK;
+    }
+    deferred.side_cu_lo = R;
+    if (deferred.side.empty()) return BAKRON_OK;
+    const int off = (int)f->items_host.size();
+    for (bk::PlanOp& op : deferred.ops) if (op.kind == 1) op.item_off += off;
+    for (bk::PlanOp& op : deferred.side) op.item_off += off;
+    f->items_host.insert(f->items_host.end(), items.begin(), items.end());
+    f->plan[1] = std::move(deferred);
+    return BAKRON_OK;
+}
+
 static bakron_status ensure_workspace(bakron_factors* f, int64_t m, int64_t n) {
     if (f->ws_m == m && f->ws_n == n && f->ws_mem) return BAKRON_OK;
     bakron_status st;
     const int64_t mt = cdiv(m, bk::TS), nt = cdiv(n, bk::TS);
     if (f->ws_mem) { hipFree(f->ws_mem); f->ws_mem = nullptr; }
     f->ws_m = f->ws_n = -1;
-    build_plan((int)mt, (int)nt, f->knear, f->b_ident, f->plan, f->items_host);
+    st = plan_with_side_stream(f, (int)mt, (int)nt);
+    if (st != BAKRON_OK) return st;
     const size_t tiles = (size_t)mt * (size_t)nt;
     const size_t fbytes = sizeof(float) * tiles * bk::TILE_ELEMS;
-    const size_t ibytes = sizeof(int) * (tiles + (size_t)f->plan.nseg + 1);
+    const size_t ibytes = sizeof(int) * (tiles + (size_t)f->plan[0].nseg + 1);
     hipError_t e = hipMalloc(&f->ws_mem, 2 * fbytes + ibytes);
     if (e != hipSuccess) return hip_fail(&f->err, e, "bakron_solve: hipMalloc (workspace)");
     char* base = static_cast<char*>(f->ws_mem);
     int* ints = reinterpret_cast<int*>(base + 2 * fbytes);
     f->ws = bk::Workspace{reinterpret_cast<float*>(base), reinterpret_cast<float*>(base + fbytes),
-                          ints, ints + tiles, ints + tiles + f->plan.nseg};
+                          ints, ints + tiles, ints + tiles + f->plan[0].nseg};
     st = ensure_identity(f, mt);
     if (st != BAKRON_OK) return st;
     if (f->items) { hipFree(f->items); f->items = nullptr; }
@@ -359,13 +520,17 @@ static bakron_status ensure_workspace(bakron_factors* f, int64_t m, int64_t n) {
         if (e != hipSuccess) return hip_fail(&f->err, e, "bakron_solve: work list upload");
     }
     // per timed launch: class and work, in plan order
-    f->tclass.assign(1, 0);
-    f->tflops.assign(1, (double)m * n * 4.0 + 2.0 * (double)fbytes);   // bytes for class 0
-    f->tmfma.assign(1, 0.0);
-    for (const bk::PlanOp& op : f->plan.ops) {
-        f->tclass.push_back(op.kind == 0 ? 1 : 2);
-        f->tflops.push_back(op.flops);
-        f->tmfma.push_back(op.mfma_flops);
+    for (int pi = 0; pi < 2; ++pi) {
+        const bk::Plan& pl = f->plan[pi];
+        f->tclass[pi].assign(1, 0);
+        f->tflops[pi].assign(1, (double)m * n * 4.0 + 2.0 * (double)fbytes);   // bytes for class 0
+        f->tmfma[pi].assign(1, 0.0);
+        for (const std::pair<int, int>& o : pl.order) {
+            const bk::PlanOp& op = o.first == 0 ? pl.ops[o.second] : pl.side[o.second];
+            f->tclass[pi].push_back(op.kind == 0 ? 1 : 2);
+            f->tflops[pi].push_back(op.flops);
+            f->tmfma[pi].push_back(op.mfma_flops);
+        }
     }
     f->ws_m = m;
     f->ws_n = n;
@@ -407,10 +572,15 @@ static bakron_status solve_impl(const float* W, int64_t m, int64_t n, const bakr
     if (st != BAKRON_OK) return st;
     const int mt = (int)cdiv(m, bk::TS), nt = (int)cdiv(n, bk::TS);
     const float qmax = (float)((1 << (q.bits - 1)) - 1);
+    // the legacy default stream synchronises implicitly with the (blocking)
+    // CU-restricted streams, so calls on it use the one-stream plan
+    const bool legacy = stream == nullptr || stream == hipStreamLegacy;
+    const int pi = (!legacy && !f->plan[1].side.empty()) ? 1 : 0;
+    f->last_plan = pi;
     hipEvent_t* tim = nullptr;
     f->prof_valid = 0;
     if (f->prof) {
-        const size_t need = 2 * (size_t)bk::plan_timed_launches(f->plan);
+        const size_t need = 2 * (size_t)bk::plan_timed_launches(f->plan[pi]);
         while (f->tim.size() < need) {
             hipEvent_t ev;
             hipError_t ee = hipEventCreate(&ev);
@@ -419,8 +589,23 @@ static bakron_status solve_impl(const float* W, int64_t m, int64_t n, const bakr
         }
         tim = f->tim.data();
     }
-    hipError_t e = bk::run_plan(stream, f->plan, W, m, n, mt, nt, f->ws, f->LA, f->LB, f->b_ident,
-                                q.scale, qmax, codes, V, pre, f->knear, f->items, tim);
+    // with side ops the main ops run on the handle's non-blocking stream,
+    // forked from and joined back into the caller's stream
+    const bool fork = pi == 1;
+    hipStream_t ms = fork ? f->main : stream;
+    hipError_t e = hipSuccess;
+    if (fork) {
+        e = hipEventRecord(f->ev_fork, stream);
+        if (e == hipSuccess) e = hipStreamWaitEvent(ms, f->ev_fork, 0);
+    }
+    if (e == hipSuccess)
+        e = bk::run_plan(ms, f->side, f->plan[pi], W, m, n, mt, nt, f->ws, f->LA, f->LB, f->b_ident,
+                         q.scale, qmax, codes, V, pre, f->knear, f->items, tim, f->ev_rel.data(),
+                         f->ev_side.data());
+    if (fork && e == hipSuccess) {
+        e = hipEventRecord(f->ev_join, ms);
+        if (e == hipSuccess) e = hipStreamWaitEvent(stream, f->ev_join, 0);
+    }
     if (e != hipSuccess) return hip_fail(&f->err, e, "bakron_solve: launch");
     f->prof_valid = f->prof;
     return BAKRON_OK;
@@ -497,17 +682,18 @@ extern "C" bakron_status bakron_profile_read(const bakron_factors* f, bakron_ker
     if (!f || !stats || nstats < 1) return BAKRON_EINVAL;
     if (!f->prof_valid) return BAKRON_EINVAL;
     for (int k = 0; k < nstats; ++k) stats[k] = bakron_kernel_stat{0.0, 0, 0.0, 0.0};
-    for (size_t i = 0; i < f->tclass.size(); ++i) {
+    const int pi = f->last_plan;
+    for (size_t i = 0; i < f->tclass[pi].size(); ++i) {
         float ms = 0.0f;
         hipError_t e = hipEventElapsedTime(&ms, f->tim[2 * i], f->tim[2 * i + 1]);
         if (e != hipSuccess)
             return hip_fail(&const_cast<bakron_factors*>(f)->err, e, "bakron_profile_read");
-        const int k = f->tclass[i];
+        const int k = f->tclass[pi][i];
         if (k >= nstats) continue;
         stats[k].ms += ms;
         stats[k].launches += 1;
-        stats[k].flops += f->tflops[i];
-        stats[k].mfma_flops += f->tmfma[i];
+        stats[k].flops += f->tflops[pi][i];
+        stats[k].mfma_flops += f->tmfma[pi][i];
     }
     return BAKRON_OK;
 }

@@ -34,30 +34,47 @@ __host__ __device__ inline int64_t ws_tile_offset(int64_t I, int64_t J, int64_t 
     return (I * nt + J) * (int64_t)TILE_ELEMS;
 }
 
-// Launch plan of one solve shape (Alg. 6 on tile anti-diagonals), all on
-// the caller's stream, in order:
+// Launch plan of one solve shape (Alg. 6 on tile anti-diagonals).  Main ops
+// run on the caller's stream, in order:
 //   segment : a divide-and-conquer subtree [K, L) no wider than KNEAR + 1
 //             tile anti-diagonals, solved by one persistent launch; each tile
 //             pulls the errors of the tiles at distance 1..KNEAR above it and
 //             to its left itself (Eq. (1)), so every (source, target) pair
 //             closer than KNEAR + 1 is applied by the target;
-//   node    : the push of a wider node, restricted to (source, target) pairs
-//             farther apart than KNEAR, as dense MFMA products.
+//   node    : the push of a wider node [K, Mid, L), restricted to (source,
+//             target) pairs farther apart than KNEAR, as dense MFMA products
+//             into the targets on [tlo, thi).
+// A node's push into its first right segment is a main op placed right after
+// its left subtree.  Its pushes into the later segments of its right subtree
+// may instead be side ops: they run on a second stream restricted to the CUs
+// the segment launches leave free, in deadline order, each after its node's
+// left subtree (main op `rel`), and every main op that touches a segment
+// first waits for the side ops targeting it (`need_side`: all side ops with
+// index below it).
 // flops = algorithmic work (2 * TS^3 per (source, target) tile pair, plus the
 // in-tile pairs of a solved tile); mfma_flops = executed on the matrix cores,
 // zero-masked tiles included.
 struct PlanOp {
     int kind;            // 0 segment, 1 node
-    int K, Mid, L;       // segment: diagonals [K, L); node: sources [K, Mid), targets [Mid, L)
+    int K, Mid, L;       // segment: diagonals [K, L); node: sources [K, Mid)
+    int tlo, thi;        // node: targets [tlo, thi)
     int strip_lo;        // segment: first tile column (strip) with a tile in [K, L)
     int nstrips;         // segment: number of such strips
     int counter;         // segment: index of its ticket counter
     int macro;           // node: solver tiles per workgroup edge (4 or 2)
     int item_off, item_cnt;
+    int rel;             // side op: main op after which it may start
+    int rec_rel;         // main op: some side op waits for it (record its event)
+    int need_side;       // main op: side ops [0, need_side) must be complete first
     double flops, mfma_flops;
 };
 struct Plan {
-    std::vector<PlanOp> ops;
+    std::vector<PlanOp> ops;    // main stream
+    std::vector<PlanOp> side;   // side stream (empty when not deferring)
+    // host enqueue order: (0, main op index) or (1, side op index); side ops
+    // are enqueued as soon as the main op they wait for has been enqueued
+    std::vector<std::pair<int, int>> order;
+    int side_cu_lo = 0;         // side stream runs on CUs [side_cu_lo, #CUs)
     int nseg = 0;
 };
 

@@ -497,7 +497,8 @@ __global__ __launch_bounds__(512) void k_seg(SegArgs a) {
 }
 
 struct NodeArgs {
-    int K, Mid, L;    // tile anti-diagonal range [K, L), split at Mid
+    int K, Mid;       // sources on tile anti-diagonals [K, Mid)
+    int tlo, thi;     // targets on tile anti-diagonals [tlo, thi)
     int knear;
     int mt, nt;
     float* X;
@@ -642,7 +643,7 @@ __global__ __launch_bounds__(256, (MT == 4 ? 2 : 4)) void k_node(NodeArgs a) {
             const int tm = wm * WB + x, tn = wn * WB + y;
             const int I = colpush ? I0 + tm : I0 + tn;
             const int J = colpush ? J0 + tn : J0 + tm;
-            if (I >= a.mt || J >= a.nt || I + J < a.Mid || I + J >= a.L) continue;
+            if (I >= a.mt || J >= a.nt || I + J < a.tlo || I + J >= a.thi) continue;
             float* out = (colpush ? a.Y : a.X) + ws_tile_offset(I, J, a.nt);
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
@@ -691,20 +692,23 @@ __global__ __launch_bounds__(256) void k_prep(const float* __restrict__ W, int64
 // ---------------------------------------------------------------------------
 // host launch driver
 
-// Launches the plan on one stream.  tim (optional, profiling): an event pair
-// around every launch, in plan order (prep first).
-hipError_t run_plan(hipStream_t st, const Plan& plan, const float* W, int64_t m, int64_t n, int mt,
-                    int nt, const Workspace& ws, const float* LA, const float* LB, int b_ident,
-                    const float* scale, float qmax, int8_t* codes, float* V, float* pre, int knear,
-                    const int4* items, hipEvent_t* tim) {
+// Launches the plan: main ops on `st`, side ops on `side` (see Plan).
+// ev_rel[i] is recorded on st after main op i when a side op waits for it;
+// ev_side[c] on `side` after side op c.  tim (optional, profiling): an event
+// pair around every launch, in enqueue order (prep first).
+hipError_t run_plan(hipStream_t st, hipStream_t side, const Plan& plan, const float* W, int64_t m,
+                    int64_t n, int mt, int nt, const Workspace& ws, const float* LA, const float* LB,
+                    int b_ident, const float* scale, float qmax, int8_t* codes, float* V, float* pre,
+                    int knear, const int4* items, hipEvent_t* tim, hipEvent_t* ev_rel,
+                    hipEvent_t* ev_side) {
     int ti = 0;
-    auto t_begin = [&]() { if (tim) hipEventRecord(tim[2 * ti], st); };
-    auto t_end = [&]() { if (tim) hipEventRecord(tim[2 * ti + 1], st); ++ti; };
+    auto t_begin = [&](hipStream_t s) { if (tim) (void)hipEventRecord(tim[2 * ti], s); };
+    auto t_end = [&](hipStream_t s) { if (tim) (void)hipEventRecord(tim[2 * ti + 1], s); ++ti; };
     hipError_t e;
-    t_begin();
+    t_begin(st);
     hipLaunchKernelGGL(k_prep, dim3((unsigned)((int64_t)mt * nt)), dim3(256), 0, st, W, m, n, mt, nt,
                        ws.X, ws.Y, ws.flags, ws.counters, plan.nseg, ws.status);
-    t_end();
+    t_end(st);
     if ((e = hipGetLastError()) != hipSuccess) return e;
 
     SegArgs sa{};
@@ -714,32 +718,56 @@ hipError_t run_plan(hipStream_t st, const Plan& plan, const float* W, int64_t m,
     sa.status = ws.status;
     NodeArgs nd{};
     nd.knear = knear; nd.mt = mt; nd.nt = nt; nd.X = ws.X; nd.Y = ws.Y; nd.LA = LA; nd.LB = LB;
-    for (const PlanOp& op : plan.ops) {
-        t_begin();
-        if (op.kind == 0) {
-            sa.K = op.K;
-            sa.L = op.L;
-            sa.J_lo = op.strip_lo;
-            sa.nstrips = op.nstrips;
-            sa.counter = ws.counters + op.counter;
-            const int grid = op.nstrips < SEG_GRID ? op.nstrips : SEG_GRID;
-            hipLaunchKernelGGL(k_seg, dim3((unsigned)grid), dim3(512), 0, st, sa);
+    auto node = [&](const PlanOp& op, hipStream_t s) {
+        nd.K = op.K;
+        nd.Mid = op.Mid;
+        nd.tlo = op.tlo;
+        nd.thi = op.thi;
+        nd.items = items + op.item_off;
+        if (op.macro == 4)
+            hipLaunchKernelGGL(k_node<4>, dim3((unsigned)op.item_cnt), dim3(256), 0, s, nd);
+        else
+            hipLaunchKernelGGL(k_node<2>, dim3((unsigned)op.item_cnt), dim3(256), 0, s, nd);
+    };
+    int waited_side = 0, waited_rel = -1;
+    for (const std::pair<int, int>& o : plan.order) {
+        if (o.first == 0) {
+            const PlanOp& op = plan.ops[o.second];
+            if (op.need_side > waited_side) {
+                if ((e = hipStreamWaitEvent(st, ev_side[op.need_side - 1], 0)) != hipSuccess) return e;
+                waited_side = op.need_side;
+            }
+            t_begin(st);
+            if (op.kind == 0) {
+                sa.K = op.K;
+                sa.L = op.L;
+                sa.J_lo = op.strip_lo;
+                sa.nstrips = op.nstrips;
+                sa.counter = ws.counters + op.counter;
+                const int grid = op.nstrips < SEG_GRID ? op.nstrips : SEG_GRID;
+                hipLaunchKernelGGL(k_seg, dim3((unsigned)grid), dim3(512), 0, st, sa);
+            } else {
+                node(op, st);
+            }
+            t_end(st);
+            if ((e = hipGetLastError()) != hipSuccess) return e;
+            if (op.rec_rel && (e = hipEventRecord(ev_rel[o.second], st)) != hipSuccess) return e;
         } else {
-            nd.K = op.K;
-            nd.Mid = op.Mid;
-            nd.L = op.L;
-            nd.items = items + op.item_off;
-            if (op.macro == 4)
-                hipLaunchKernelGGL(k_node<4>, dim3((unsigned)op.item_cnt), dim3(256), 0, st, nd);
-            else
-                hipLaunchKernelGGL(k_node<2>, dim3((unsigned)op.item_cnt), dim3(256), 0, st, nd);
+            const PlanOp& op = plan.side[o.second];
+            if (op.rel > waited_rel) {
+                if ((e = hipStreamWaitEvent(side, ev_rel[op.rel], 0)) != hipSuccess) return e;
+                waited_rel = op.rel;
+            }
+            t_begin(side);
+            node(op, side);
+            t_end(side);
+            if ((e = hipGetLastError()) != hipSuccess) return e;
+            if ((e = hipEventRecord(ev_side[o.second], side)) != hipSuccess) return e;
         }
-        t_end();
-        if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     return hipSuccess;
 }
 
-int plan_timed_launches(const Plan& plan) { return 1 + (int)plan.ops.size(); }
+int plan_timed_launches(const Plan& plan) { return 1 + (int)plan.ops.size() + (int)plan.side.size(); }
 
 }  // namespace bk

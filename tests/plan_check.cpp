@@ -1,0 +1,106 @@
+// CPU check of the launch plans (Alg. 6 over tile anti-diagonals, as built
+// by csrc/api.hip): every (source, target) tile pair farther than knear apart
+// is applied exactly once, by a node push whose sources are solved before it
+// and whose targets are solved after it; side-stream pushes are released after
+// their sources, waited for before any main op that writes their targets, and
+// never run while a main op writes the same tiles; the host enqueue order
+// respects every wait.  The launch functions are stubbed out: only the host
+// planning code runs.  Exit status = number of failing cases.
+#include "api.hip"
+#include <cstdio>
+#include <map>
+#include <set>
+#include <tuple>
+int check(int mt, int nt, int knear, int b_ident, bool defer) {
+    bk::Plan plan; std::vector<int4> items;
+    build_plan(mt, nt, knear, b_ident, defer, plan, items);
+    const int Q = mt + nt - 1;
+    std::vector<int> seg_pos(Q, -1);
+    for (int i = 0; i < (int)plan.ops.size(); ++i)
+        if (plan.ops[i].kind == 0) for (int D = plan.ops[i].K; D < plan.ops[i].L; ++D) seg_pos[D] = i;
+    for (int D = 0; D < Q; ++D) if (seg_pos[D] < 0) { printf("diag %d unsolved\n", D); return 1; }
+    // first main op that waits for side op c
+    std::vector<int> first_wait(plan.side.size(), (int)plan.ops.size());
+    for (int i = (int)plan.ops.size() - 1; i >= 0; --i)
+        for (int c = 0; c < plan.ops[i].need_side; ++c) first_wait[c] = i;
+    std::map<std::tuple<int,int,int,int>, int> cnt;
+    int bad = 0;
+    // lo < pos < hi in main-op time: source segment <= lo, target segment >= hi
+    auto apply = [&](int lo, int hi, const bk::PlanOp& op, int4 it) {
+        const int I0 = it.x, J0 = it.y, kind = it.z & 1, klo = it.z >> 1, khi = it.w, MT = op.macro;
+        for (int a = 0; a < MT; ++a) for (int b = 0; b < MT; ++b) {
+            int I = I0 + a, J = J0 + b;
+            if (I >= mt || J >= nt || I + J < op.tlo || I + J >= op.thi) continue;
+            for (int kt = klo; kt < khi; ++kt) {
+                int sd;
+                if (kind == 0) { if (!(kt <= I - knear - 1) || !(kt + J >= op.K && kt + J < op.Mid)) continue; sd = kt + J; }
+                else { if (!(kt <= J - knear - 1) || !(I + kt >= op.K && I + kt < op.Mid)) continue; sd = I + kt; }
+                if (b_ident && kind == 0) continue;
+                cnt[{kind, I, J, kt}]++;
+                if (!(seg_pos[sd] <= lo) || !(hi <= seg_pos[I + J])) {
+                    if (bad < 5) printf("order error kind %d tgt (%d,%d) src %d lo %d hi %d sp %d tp %d\n", kind, I, J, kt, lo, hi, seg_pos[sd], seg_pos[I + J]);
+                    ++bad;
+                }
+            }
+        }
+    };
+    for (int i = 0; i < (int)plan.ops.size(); ++i) {
+        const bk::PlanOp& op = plan.ops[i];
+        if (op.kind == 1)
+            for (int j = 0; j < op.item_cnt; ++j) apply(i - 1, i + 1, op, items[op.item_off + j]);
+        // a main op never runs before the side ops its targets need
+        for (int c = 0; c < (int)plan.side.size(); ++c) {
+            const bk::PlanOp& so = plan.side[c];
+            const bool overlap = op.tlo < so.thi && so.tlo < op.thi;
+            if (overlap && i > so.rel && i < first_wait[c]) { if (bad < 5) printf("race: main %d with side %d\n", i, c); ++bad; }
+        }
+    }
+    for (int c = 0; c < (int)plan.side.size(); ++c) {
+        const bk::PlanOp& so = plan.side[c];
+        if (!plan.ops[so.rel].rec_rel) { printf("side %d: release not recorded\n", c); ++bad; }
+        for (int j = 0; j < so.item_cnt; ++j) apply(so.rel, first_wait[c], so, items[so.item_off + j]);
+    }
+    // enqueue order: every side op after its release op, main ops in order
+    {
+        std::vector<int> seen_main;
+        int last_main = -1;
+        for (auto& o : plan.order) {
+            if (o.first == 0) { if (o.second != last_main + 1) { printf("main order\n"); ++bad; } last_main = o.second; }
+            else if (plan.side[o.second].rel > last_main) { printf("side %d enqueued before its release\n", o.second); ++bad; }
+        }
+        // every waited side op is enqueued before the waiting main op
+        std::vector<int> pos_side(plan.side.size(), -1), pos_main(plan.ops.size(), -1);
+        for (int k = 0; k < (int)plan.order.size(); ++k) (plan.order[k].first ? pos_side : pos_main)[plan.order[k].second] = k;
+        for (int i = 0; i < (int)plan.ops.size(); ++i)
+            for (int c = 0; c < plan.ops[i].need_side; ++c)
+                if (pos_side[c] > pos_main[i]) { printf("main %d waits for side %d enqueued later\n", i, c); ++bad; }
+    }
+    long missing = 0, dup = 0, expected = 0, extra = 0;
+    for (int I = 0; I < mt; ++I) for (int J = 0; J < nt; ++J) {
+        for (int kt = 0; kt < I - knear; ++kt) { if (b_ident) break; ++expected; auto c = cnt[{0, I, J, kt}]; if (c == 0) ++missing; if (c > 1) ++dup; }
+        for (int kt = 0; kt < J - knear; ++kt) { ++expected; auto c = cnt[{1, I, J, kt}]; if (c == 0) ++missing; if (c > 1) ++dup; }
+    }
+    for (auto& kv : cnt) { auto [kind, I, J, kt] = kv.first; if (kind == 0 ? kt > I - knear - 1 : kt > J - knear - 1) ++extra; }
+    int nnode = 0; for (auto& op : plan.ops) nnode += op.kind == 1;
+    if (missing || dup || extra || bad || (mt == 128 && nt == 128 && knear == 8))
+        printf("mt %d nt %d knear %d bident %d defer %d: main %zu (nodes %d) side %zu; far pairs %ld missing %ld dup %ld extra %ld errors %d\n",
+               mt, nt, knear, b_ident, (int)defer, plan.ops.size(), nnode, plan.side.size(), expected, missing, dup, extra, bad);
+    return (missing || dup || extra || bad) ? 1 : 0;
+}
+int main() {
+    int fails = 0;
+    int small[][2] = {{1,1},{2,3},{7,10},{10,7},{6,6},{9,5},{40,40},{70,33},{33,90}};
+    for (auto& sh : small) for (int k : {0, 1, 3, 8}) for (int bi : {0, 1}) for (int d : {0, 1})
+        fails += check(sh[0], sh[1], k, bi, d);
+    for (int k : {1, 8}) for (int d : {0, 1}) fails += check(128, 128, k, 0, d);   // the 4096^2 layer
+    printf("fails %d\n", fails);
+    return fails;
+}
+namespace bk {
+hipError_t factor_one(hipStream_t, const float*, int64_t, double, double*, double*, double*, double*, int*, int64_t*, float*, int64_t) { return hipSuccess; }
+hipError_t pack_identity(hipStream_t, int64_t, float*) { return hipSuccess; }
+hipError_t unpack_factor(hipStream_t, const float*, int64_t, float*) { return hipSuccess; }
+int plan_timed_launches(const Plan&) { return 0; }
+hipError_t run_plan(hipStream_t, hipStream_t, const Plan&, const float*, int64_t, int64_t, int, int, const Workspace&, const float*, const float*, int, const float*, float, int8_t*, float*, float*, int, const int4*, hipEvent_t*, hipEvent_t*, hipEvent_t*) { return hipSuccess; }
+hipError_t run_antidiag(hipStream_t, const float*, int64_t, int64_t, float*, float*, const float*, const float*, const float*, float, int8_t*, float*, float*) { return hipSuccess; }
+}

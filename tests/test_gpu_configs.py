@@ -1,4 +1,6 @@
-"""Full-size configurations, in the launch configuration bench.py times.
+"""Full-size configurations, in the launch configuration bench.py times (a
+stream of its own, where node pushes into later segments overlap with the
+segment launches on a CU-restricted side stream).
 
 At these sizes the sequential oracle cannot replay every entry, so parity is
 checked two ways:
@@ -20,6 +22,13 @@ from gpu_util import TIE_WINDOW, MAX_FLIP_RATE, gpu_run, log, v_is_scale_times_c
 pytestmark = [pytest.mark.gpu, pytest.mark.slow]
 
 
+def _run(p, debug):
+    """gpu_run on a non-default stream, as bench.py runs the solver."""
+    import torch
+    with torch.cuda.stream(torch.cuda.Stream()):
+        return gpu_run(p, debug=debug)
+
+
 def _rows(m, full):
     if full:
         return None
@@ -36,7 +45,7 @@ def test_config_certificate(oracle_mod, cid):
     c = workloads.make(cid, seed=0, device="cuda")
     m, n = c["W"].shape
     log(f"case config {cid}: solving {m}x{n}")
-    codes, V, pre = gpu_run(c)
+    codes, V, pre = _run(c, True)
     assert v_is_scale_times_code(V, codes, c["scale"])
     l = (1 << (c["bits"] - 1)) - 1
     assert np.all(np.abs(codes.astype(np.int32)) <= l)
@@ -62,10 +71,24 @@ def test_config_shape_ar1_exact(oracle_mod, cid):
     p = dict(W=W, A=workloads.ar1_toeplitz(cfg.n, 0.5), B=workloads.ar1_toeplitz(cfg.m, 0.25),
              scale=s, bits=cfg.bits, damp=0.0)
     log(f"case AR(1) at config {cid} shape {cfg.m}x{cfg.n}")
-    codes, V, pre = gpu_run(p, debug=False)
+    codes, V, pre = _run(p, False)
     r = oracle_mod.ar1_diffusion(W, 0.5, 0.25, s, cfg.bits, forced=codes, tie_window=TIE_WINDOW)
     viol = int(np.count_nonzero(r["codes"] != codes))
     log(f"[ar1 config{cid}] violations={viol} flips={r['n_flip']} excused={r['n_excused']}")
     assert viol == 0
     assert r["n_flip"] <= MAX_FLIP_RATE * W.size
     assert v_is_scale_times_code(V, codes, s)
+
+
+@pytest.mark.timeout(600)
+def test_config2_two_stream_plan_bitwise():
+    """The 4096x4096 layer on a stream of its own (node pushes overlapped on the
+    side stream) and on the legacy default stream (everything on one stream):
+    bitwise identical codes, V and pre-rounding values."""
+    c = workloads.make(2, seed=0, device="cuda")
+    log("case config 2 two-stream vs one-stream plan")
+    c1, v1, x1 = _run(c, True)
+    c0, v0, x0 = gpu_run(c, debug=True)
+    assert np.array_equal(c0, c1)
+    assert np.array_equal(v0.view(np.uint32), v1.view(np.uint32))
+    assert np.array_equal(x0.view(np.uint32), x1.view(np.uint32))

@@ -93,3 +93,34 @@ def test_ar1_structured_exact(oracle_mod):
     r = oracle_mod.ar1_diffusion(W, 0.5, 0.25, p["scale"], 3, forced=codes, tie_window=1e-4)
     assert np.count_nonzero(r["codes"] != codes) == 0
     assert r["n_flip"] <= 1e-4 * m * n
+
+
+@pytest.mark.parametrize("m,n,k", [(600, 500, 8), (300, 420, 1)])
+def test_side_stream_bitwise(m, n, k):
+    """On a non-default stream, node pushes into later segments run on a
+    CU-restricted side stream (BAKRON_DEFER, read when a handle first plans a
+    shape); on the legacy default stream and with BAKRON_DEFER=0 everything
+    runs on the caller's stream.  Every target tile receives the same
+    additions in the same order either way, so the results must be bitwise
+    identical."""
+    import os
+    import torch
+    p = _problem(m, n, seed=m + 3 * n)
+    log(f"case side stream m={m} n={n} knear={k}")
+    old = os.environ.get("BAKRON_DEFER")
+    try:
+        os.environ["BAKRON_DEFER"] = "0"
+        c0, v0, x0 = gpu_run(p, k=k)
+        os.environ["BAKRON_DEFER"] = "1"
+        with torch.cuda.stream(torch.cuda.Stream()):
+            c1, v1, x1 = gpu_run(p, k=k, repeat=2)[1]
+        c2, v2, x2 = gpu_run(p, k=k)
+    finally:
+        if old is None:
+            os.environ.pop("BAKRON_DEFER", None)
+        else:
+            os.environ["BAKRON_DEFER"] = old
+    for c, v, x in ((c1, v1, x1), (c2, v2, x2)):
+        assert np.array_equal(c0, c)
+        assert np.array_equal(v0.view(np.uint32), v.view(np.uint32))
+        assert np.array_equal(x0.view(np.uint32), x.view(np.uint32))
