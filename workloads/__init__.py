@@ -21,6 +21,11 @@ available here, so these LLM-shaped synthetic layers stand in for them:
 
 RNG: numpy PCG64 seeded by SeedSequence([config_id, seed, stream]) with
 streams W=0, X(for A)=1, G(for B)=2, spike=3, outliers=4.
+
+Calibration samples for the Kronecker-factor construction (App. A) come from
+kron_samples (global case: inputs a and output gradients b) and mlp_samples
+(gated MLP: inputs x, weights, features g and f), with *_torch versions of the
+same recipes for full-size workloads drawn on the GPU.
 """
 from __future__ import annotations
 
@@ -113,6 +118,108 @@ def gram_ar1(d: int, N: int, rho: float, rng: np.random.Generator, spike_rank: i
         G = G.cpu().numpy()
     G /= float(N)
     return 0.5 * (G + G.T)
+
+
+def ar1_samples(N: int, d: int, rho: float, rng: np.random.Generator, spike_rank: int = 0,
+                spike_rng: np.random.Generator | None = None,
+                norm_sigma: float = 0.0) -> np.ndarray:
+    """N calibration samples as the rows of an N x d fp32 matrix: each an
+    AR(1) sequence along the feature index (the recipe of gram_ar1), plus an
+    optional rank-r spike, times an optional per-sample log-normal magnitude
+    exp(norm_sigma * z_k) (tokens and gradients of very different norms)."""
+    c = np.sqrt(1.0 - rho * rho)
+    eps = rng.standard_normal((N, d))
+    X = np.empty((N, d), np.float64)
+    X[:, 0] = eps[:, 0]
+    for t in range(1, d):
+        X[:, t] = rho * X[:, t - 1] + c * eps[:, t]
+    if spike_rank > 0:
+        q, _ = np.linalg.qr(spike_rng.standard_normal((d, spike_rank)))
+        X += (spike_rng.standard_normal((N, spike_rank)) * np.sqrt(10.0)) @ q.T
+    if norm_sigma > 0:
+        X *= np.exp(norm_sigma * rng.standard_normal((N, 1)))
+    return X.astype(np.float32)
+
+
+def kron_samples(N: int, n: int, m: int, seed: int) -> dict:
+    """Paired samples of a global Hessian: inputs a (N x n: AR(1), rho 0.5,
+    rank-4 spike, log-normal token norms sigma 0.5) and output gradients b
+    (N x m: AR(1), rho 0.2, log-normal norms sigma 1.0), fp32."""
+    r = [np.random.Generator(np.random.PCG64(np.random.SeedSequence([2000, N, n, m, seed, k])))
+         for k in range(3)]
+    a = ar1_samples(N, n, 0.5, r[0], spike_rank=min(4, n), spike_rng=r[2], norm_sigma=0.5)
+    b = ar1_samples(N, m, 0.2, r[1], norm_sigma=1.0)
+    return dict(a=a, b=b)
+
+
+def mlp_samples(N: int, dm: int, dff: int, seed: int) -> dict:
+    """A gated MLP, MLP(x) = W_down (W_up x (.) SiLU(W_gate x)), with Gaussian
+    weights (W_gate, W_up ~ N(0, 1/dm), W_down ~ N(0, 1/dff)) and inputs x as
+    in kron_samples; the features g = SiLU(W_gate x) and
+    f = SiLU'(W_gate x) (.) W_up x are this forward pass, in fp64, rounded
+    once to fp32 (the module's own computation, not the Hessian's)."""
+    r = [np.random.Generator(np.random.PCG64(np.random.SeedSequence([3000, N, dm, dff, seed, k])))
+         for k in range(3)]
+    x = ar1_samples(N, dm, 0.5, r[0], spike_rank=min(4, dm), spike_rng=r[2], norm_sigma=0.5)
+    Wg = r[1].standard_normal((dff, dm)) / np.sqrt(dm)
+    Wu = r[1].standard_normal((dff, dm)) / np.sqrt(dm)
+    Wd = r[1].standard_normal((dm, dff)) / np.sqrt(dff)
+    z = x.astype(np.float64) @ Wg.T
+    u = x.astype(np.float64) @ Wu.T
+    sg = 1.0 / (1.0 + np.exp(-z))
+    g = z * sg
+    f = sg * (1.0 + z * (1.0 - sg)) * u
+    return dict(x=x, Wg=Wg.astype(np.float32), Wu=Wu.astype(np.float32),
+                Wd=Wd.astype(np.float32), g=g.astype(np.float32), f=f.astype(np.float32))
+
+
+def ar1_samples_torch(N: int, d: int, rho: float, gen, device, spike_rank: int = 0,
+                      norm_sigma: float = 0.0):
+    """The recipe of ar1_samples drawn with torch's generator `gen` on `device`
+    in fp32 (for full-size workloads; different random numbers from the numpy
+    version).  Returns an N x d contiguous fp32 tensor."""
+    import torch
+    eps = torch.randn((d, N), generator=gen, device=device)
+    c = float(np.sqrt(1.0 - rho * rho))
+    for t in range(1, d):   # feature-major rows: the recursion along the feature index
+        eps[t].mul_(c).add_(eps[t - 1], alpha=rho)
+    if spike_rank > 0:
+        q, _ = torch.linalg.qr(torch.randn((d, spike_rank), generator=gen, device=device))
+        eps.addmm_(q, torch.randn((spike_rank, N), generator=gen, device=device) * np.sqrt(10.0))
+    if norm_sigma > 0:
+        eps.mul_(torch.exp(norm_sigma * torch.randn((1, N), generator=gen, device=device)))
+    X = eps.t().contiguous()
+    del eps
+    return X
+
+
+def kron_samples_torch(N: int, n: int, m: int, seed: int, device) -> dict:
+    """kron_samples' recipe on the device (torch generator seeded by seed)."""
+    import torch
+    gen = torch.Generator(device=device).manual_seed(2000 + seed)
+    a = ar1_samples_torch(N, n, 0.5, gen, device, spike_rank=min(4, n), norm_sigma=0.5)
+    b = ar1_samples_torch(N, m, 0.2, gen, device, norm_sigma=1.0)
+    return dict(a=a, b=b)
+
+
+def mlp_samples_torch(N: int, dm: int, dff: int, seed: int, device, feature: str = "g") -> dict:
+    """mlp_samples' recipe on the device in fp32, with only the requested
+    feature ("g" for W_up, "f" for W_gate)."""
+    import torch
+    gen = torch.Generator(device=device).manual_seed(3000 + seed)
+    x = ar1_samples_torch(N, dm, 0.5, gen, device, spike_rank=min(4, dm), norm_sigma=0.5)
+    Wg = torch.randn((dff, dm), generator=gen, device=device) / np.sqrt(dm)
+    Wu = torch.randn((dff, dm), generator=gen, device=device) / np.sqrt(dm)
+    Wd = (torch.randn((dm, dff), generator=gen, device=device) / np.sqrt(dff)).contiguous()
+    z = x @ Wg.t()
+    if feature == "g":
+        feat = torch.nn.functional.silu(z, inplace=True)
+    else:
+        sg = torch.sigmoid(z)
+        z.mul_(1.0 - sg).add_(1.0).mul_(sg)        # SiLU'(z) = sg (1 + z (1 - sg))
+        del sg
+        feat = z.mul_(x @ Wu.t())
+    return dict(x=x, Wg=Wg, Wu=Wu, Wd=Wd, feat=feat.contiguous())
 
 
 def make_weights(cfg: Config, seed: int) -> np.ndarray:
