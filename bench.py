@@ -162,6 +162,185 @@ def table3(max_antidiag_elems: int):
             f"{r['paper_s']['speedup']:.1f}x |")
 
 
+# Kronecker-factor construction (App. A) at the paper's calibration size:
+# 256 sequences x 2048 tokens (App. D), on Llama-3-8B's MLP and on a 4096 x 4096
+# projection with a backpropagated (global) Hessian.
+FACTOR_N = 256 * 2048
+FACTOR_WORKLOADS = (("mlp-local-up-4096x14336", "kfac"), ("mlp-local-up-4096x14336", "shampoo"),
+                    ("global-4096x4096", "kfac"), ("global-4096x4096", "shampoo"))
+
+
+def _gram_flops(N: int, d: int) -> float:
+    """Algorithmic flops of one Gram over N samples of dimension d: a multiply
+    and an add per sample for each of the d (d + 1) / 2 distinct entries."""
+    return float(N) * d * (d + 1)
+
+
+def factors_bench(steps: int, warmup: int, n_samples: int, cpu_seconds: float, do_cpu: bool):
+    """One JSON line per Kronecker-factor workload: the whole factor
+    construction per step (every Gram, weight and mask of the pair), the
+    dominant Gram launch timed alone for the roofline, 48 entries of each
+    factor checked against the fp64 oracle, and the oracle's own CPU rate."""
+    import numpy as np
+    import torch
+    import paper_2608_06291_amd as pk
+    import workloads
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.Stream(dev)
+    torch.cuda.set_stream(stream)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    N = n_samples
+    cache = {}
+    for name, style in FACTOR_WORKLOADS:
+        if name not in cache:
+            cache.clear()
+            torch.cuda.empty_cache()
+            log(f"[factors] generating {name}, N = {N}")
+            if name.startswith("mlp"):
+                p = workloads.mlp_samples_torch(N, 4096, 14336, 0, dev, "g")
+                cache[name] = (p["x"], p["feat"], p["Wd"])
+                del p
+            else:
+                p = workloads.kron_samples_torch(N, 4096, 4096, 0, dev)
+                cache[name] = (p["a"], p["b"], None)
+            torch.cuda.synchronize()
+        a, b, D = cache[name]
+        n, m = a.shape[1], b.shape[1]
+        if D is not None:
+            run = lambda: pk.mlp_local_factors(a, b, D, style)  # noqa: E731
+            # D^T D over the dm rows of D, then the two N-sample Grams
+            F = _gram_flops(D.shape[0], m) + _gram_flops(N, n) + _gram_flops(N, m)
+        else:
+            run = lambda: pk.kron_factors(a, b, style)  # noqa: E731
+            F = _gram_flops(N, n) + _gram_flops(N, m)
+        for _ in range(warmup):
+            A, B = run()
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(steps):
+            A, B = run()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / steps
+        # the dominant launch pair: the Gram of the wider operand b over N samples
+        # (k_gram and its slice reduction; the mask and weights as in the step)
+        w = pk.sample_weights(a) if style == "shampoo" else None
+        M = None
+        if D is not None:
+            M = pk.gram(D, None, 1.0)
+        C = torch.empty((m, m), dtype=torch.float32, device=dev)
+        work = torch.empty(pk.gram_workspace_bytes(N, m), dtype=torch.uint8, device=dev)
+        pk.gram(b, w, 1.0 / N, M, C, work)
+        torch.cuda.synchronize()
+        reps = max(2, steps)
+        e0.record(stream)
+        for _ in range(reps):
+            pk.gram(b, w, 1.0 / N, M, C, work)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        g_ms = e0.elapsed_time(e1) / reps
+        g_tf = _gram_flops(N, m) / (g_ms * 1e-3) / 1e12
+        # sampled parity: 48 entries of A and B against the fp64 oracle
+        import oracle
+        h = oracle.hessian
+        rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([5000, n, m])))
+
+        def pairs(d):
+            pr = [(int(i), int(j)) for i, j in rng.integers(0, d, (40, 2))]
+            return pr + [(i, i) for i in rng.integers(0, d, 8).tolist()]
+
+        def cols(X, pr):
+            idx = sorted({i for q in pr for i in q})
+            sub = X[:, idx].double().cpu().numpy()
+            pos = {c: t for t, c in enumerate(idx)}
+            return sub, [(pos[i], pos[j]) for i, j in pr]
+
+        def wts(X, c=None):   # Shampoo weights tr(.) of every sample, fp64 on the CPU
+            out = np.empty(X.shape[0])
+            for k0 in range(0, X.shape[0], 16384):
+                blk = X[k0:k0 + 16384].double().cpu().numpy()
+                out[k0:k0 + 16384] = h.trace_quad(blk[:, :, None] * (1.0 if c is None else
+                                                                      np.sqrt(c)[None, :, None]))
+            return out
+
+        pa, pb = pairs(n), pairs(m)
+        wA = wB = None
+        if style == "shampoo":
+            if D is not None:
+                Dn = D.double().cpu().numpy()
+                wA = wts(b, np.sum(Dn * Dn, axis=0))   # g^T diag(D^T D) g
+            else:
+                wA = wts(b)
+            wB = wts(a)
+        sa, qa = cols(a, pa)
+        sb, qb = cols(b, pb)
+        eA = h.expect_outer_entries(sa, qa, wA)
+        eB = h.expect_outer_entries(sb, qb, wB)
+        if D is not None:
+            sd, qd = cols(D, pb)
+            eB = eB * D.shape[0] * h.expect_outer_entries(sd, qd)
+        gA = np.array([A[i, j].item() for i, j in pa])
+        gB = np.array([B[i, j].item() for i, j in pb])
+        rel = float(max(np.max(np.abs(gA - eA) / np.abs(eA).max()),
+                        np.max(np.abs(gB - eB) / np.abs(eB).max())))
+        cpu = None
+        if do_cpu:
+            cpu = factors_cpu_baseline(a, b, D, style, F, cpu_seconds)
+        out = {
+            "metric": "Kronecker-factor construction TFLOP/s (App. A), 1 MI355X",
+            "value": F / (ms * 1e-3) / 1e12, "unit": "TFLOP/s", "n_gpus": 1, "steps": steps,
+            "warmup": warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+            "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+            "config": {"workload": f"{name}-{style}", "samples": N, "n": n, "m": m,
+                       "algorithmic_flops": F, "sampled_max_rel_err": rel},
+            "roofline": {"kernel": "k_gram + k_gram_reduce (Gram of the N x %d operand)" % m,
+                         "bound": "mfma", "achieved": g_tf, "peak": PEAK_FP32_MFMA,
+                         "unit": "TFLOP/s", "frac": g_tf / PEAK_FP32_MFMA, "traffic": None,
+                         "launch_ms": g_ms},
+            "cpu_baseline": cpu,
+        }
+        print(json.dumps(out), flush=True)
+        log(f"[factors] {name} {style}: {ms:.1f} ms/step, {out['value']:.1f} TFLOP/s; "
+            f"Gram {g_ms:.1f} ms = {g_tf:.1f} TFLOP/s ({100 * g_tf / PEAK_FP32_MFMA:.0f}% of fp32 "
+            f"MFMA peak); sampled rel err {rel:.2e}")
+        del A, B, C, work, M, w
+    cache.clear()
+
+
+def factors_cpu_baseline(a, b, D, style, F, seconds):
+    """Time the fp64 oracle on the first samples of the same workload
+    (K-FAC / Shampoo factors from its per-sample definitions, the MLP-local b
+    formed explicitly) and extrapolate linearly in the number of samples."""
+    import oracle
+    h = oracle.hessian
+    N = a.shape[0]
+    k = 1
+    while True:
+        sa = a[:k].double().cpu().numpy()
+        sb = b[:k].double().cpu().numpy()
+        t0 = time.perf_counter()
+        if D is not None:
+            h.mlp_local_factors(sa, sb, D.double().cpu().numpy(), style)
+        elif style == "kfac":
+            h.kfac_factors(sa, sb)
+        else:
+            h.shampoo_factors(sa, sb, iters=1)
+        t = time.perf_counter() - t0
+        if t >= seconds / 4 or k >= N:
+            break
+        k = min(N, max(k * 2, int(k * seconds / 4 / max(t, 1e-3))))
+    t_full = t * N / k
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:
+        cores = 1
+    return dict(value=F / t_full / 1e12, unit="TFLOP/s", cores=cores, kind="oracle",
+                sample=f"first {k} of {N} samples of the same workload, {t:.1f} s measured; "
+                       f"extrapolated linearly in the sample count",
+                s_per_step=t_full, host_cpu=cpu_model())
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -180,6 +359,11 @@ def main():
                          "BaKron-antidiagonal) and exit; one JSON line per shape")
     ap.add_argument("--table3-max-antidiag-elems", type=int, default=1 << 27,
                     help="skip BaKron-antidiagonal (quartic work) above this many matrix entries")
+    ap.add_argument("--factors", action="store_true",
+                    help="only run the Kronecker-factor construction workloads (App. A: K-FAC and "
+                         "single-step Shampoo, global and MLP-local) and exit; one JSON line each")
+    ap.add_argument("--factor-samples", type=int, default=FACTOR_N,
+                    help="calibration samples for --factors (default 256 x 2048)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: --gpus {args.gpus} is not supported: the BaKron solve runs on one "
@@ -192,6 +376,11 @@ def main():
 
     if args.table3:
         table3(args.table3_max_antidiag_elems)
+        return
+
+    if args.factors:
+        factors_bench(args.steps, args.warmup, args.factor_samples, args.cpu_seconds,
+                      not args.no_cpu_baseline)
         return
 
     if args.copy_calibration_mib > 0:

@@ -197,6 +197,102 @@ bakron_status bakron_profile_read(const bakron_factors *f, bakron_kernel_stat *s
  */
 bakron_status bakron_solve_check(const bakron_factors *f, hipStream_t stream, int32_t *failed);
 
+/* ------------------------------------------------------------------------
+ * Kronecker-factor construction from calibration samples (Sec. 4, App. A).
+ *
+ * The Hessian of a linear unit W (m x n) is an expectation of Kronecker
+ * products, H = E[a a^T (x) b b^T], a the unit's input, b the gradient of the
+ * loss with respect to its output (global case, both vectors) or the
+ * MLP-local matrix b = D_g W_down^T.  Two Kronecker approximations H ~ A (x) B
+ * are formed (App. A):
+ *   K-FAC style     A = E[a a^T],               B = E[b b^T];
+ *   Shampoo style   one power-iteration step of the best Kronecker
+ *                   approximation (rearrangement of H) from A0 = I, B0 = I:
+ *                   A = E[tr(b^T b) a a^T],     B = E[tr(a^T a) b b^T].
+ * E is the sample mean (1/N) sum_k.  All of them reduce to one primitive,
+ * the weighted masked Gram matrix C = s * (X^T diag(w) X) (.) M.
+ *
+ * Conventions of this group (in addition to those above):
+ *   - sample matrices are N x d row-major fp32, one sample per row;
+ *   - computed in fp32 on the matrix cores (fp32 products, fp32 sums); the
+ *     summation order is fixed for a given device and shape, so repeated calls
+ *     give bitwise the same result;
+ *   - workspace protocol: with work == NULL the call stores the number of
+ *     workspace bytes it needs in *work_bytes and does nothing else (no GPU
+ *     work, pointers not checked); otherwise work is a device buffer of
+ *     *work_bytes >= that size, 256-byte aligned, owned by the caller, which
+ *     must not use it until the enqueued work completes.  The size depends on
+ *     the sizes and on the CU count of the current device;
+ *   - asynchronous on `stream`; error messages via bakron_last_error().
+ * ------------------------------------------------------------------------ */
+
+typedef enum {
+    BAKRON_KFAC = 0,     /* A = E[a a^T],           B = E[b b^T]           */
+    BAKRON_SHAMPOO = 1   /* A = E[tr(b^T b) a a^T], B = E[tr(a^T a) b b^T] */
+} bakron_kron_style;
+
+/*
+ * bakron_gram -- C = s * (X^T diag(w) X) (.) M, i.e.
+ *   C_ij = s * M_ij * sum_k w_k X_ki X_kj      (i, j < d)
+ * the Gram accumulation of the Hessian factors (Sec. 4; App. A).
+ *
+ *   X   device, N x d;  N >= 0 (N = 0 gives C = 0), 0 <= d <= 2^17
+ *   w   device, N per-sample weights, or NULL for w = 1
+ *   s   scale (1/N for a sample mean)
+ *   M   device, d x d entrywise factor, or NULL for M = 1; may be the same
+ *       buffer as C (then it is overwritten with the result)
+ *   C   device, d x d output, both triangles written
+ * Two launches.  Errors: BAKRON_EINVAL for bad sizes, NULL X (N, d > 0) or C
+ * (d > 0), or a bad workspace.
+ */
+bakron_status bakron_gram(const float *X, int64_t N, int64_t d, const float *w, float s,
+                          const float *M, float *C, void *work, size_t *work_bytes,
+                          hipStream_t stream);
+
+/*
+ * bakron_sample_weights -- w_k = sum_i c_i X_ki^2 for k < N: the per-sample
+ * Shampoo weights of App. A (c = NULL: tr(a^T a) = |a_k|^2 of vector
+ * samples; c = diag(W_down^T W_down): the MLP-local tr(b^T b) =
+ * g^T diag(W_down^T W_down) g).
+ *   X  device, N x d;  c  device, d floats, or NULL for c = 1;  w  device, N.
+ * One launch, no workspace.
+ */
+bakron_status bakron_sample_weights(const float *X, int64_t N, int64_t d, const float *c, float *w,
+                                    hipStream_t stream);
+
+/*
+ * bakron_kron_factors -- Kronecker factors of a global (backpropagated)
+ * Hessian from N paired vector samples (Sec. 4; App. A):
+ *   a  device, N x n (inputs of the unit)
+ *   b  device, N x m (gradients at the unit's output)
+ *   style  bakron_kron_style
+ *   A  device, n x n output;  B  device, m x m output
+ * N >= 1, n, m in [1, 2^17].  Workspace as above.
+ */
+bakron_status bakron_kron_factors(const float *a, const float *b, int64_t N, int64_t n, int64_t m,
+                                  int32_t style, float *A, float *B, void *work, size_t *work_bytes,
+                                  hipStream_t stream);
+
+/*
+ * bakron_mlp_local_factors -- Kronecker factors of the MLP-local Hessians of
+ * a gated MLP, MLP(x) = W_down (W_up x (.) sigma(W_gate x)) (App. A):
+ *   H_up   = E[x x^T (x) (g g^T (.) W_down^T W_down)],  g = sigma(W_gate x)
+ *   H_gate = E[x x^T (x) (f f^T (.) W_down^T W_down)],  f = sigma'(W_gate x) (.) W_up x
+ * i.e. b = D_g W_down^T, b b^T = g g^T (.) D^T D and tr(b^T b) =
+ * g^T diag(D^T D) g, with D = W_down:
+ *   K-FAC:    A = E[x x^T],                  B = E[g g^T] (.) D^T D
+ *   Shampoo:  A = E[(g^T diag(D^T D) g) x x^T], B = E[|x|^2 g g^T] (.) D^T D
+ *
+ *   x  device, N x dm (inputs of the MLP)
+ *   g  device, N x dff: the features g (for W_up) or f (for W_gate)
+ *   D  device, dm x dff: W_down
+ *   A  device, dm x dm output;  B  device, dff x dff output
+ * N >= 1, dm, dff in [1, 2^17].  Workspace as above.
+ */
+bakron_status bakron_mlp_local_factors(const float *x, const float *g, const float *D, int64_t N,
+                                       int64_t dm, int64_t dff, int32_t style, float *A, float *B,
+                                       void *work, size_t *work_bytes, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

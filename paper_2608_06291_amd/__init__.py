@@ -4,5 +4,7 @@ The solver itself is hand-written HIP for gfx950 behind a C ABI
 (``include/bakron.h``); this package only marshals arguments.
 """
 from ._lib import (BAKRON_EHIP, BAKRON_EINVAL, BAKRON_ENOMEM, BAKRON_ENOTSPD, BAKRON_OK,  # noqa: F401
-                   EXPORTED, LIB_PATH, BakronError, Factors, factor, load, solve, solve_antidiag,
+                   BAKRON_KFAC, BAKRON_SHAMPOO,
+                   EXPORTED, LIB_PATH, BakronError, Factors, factor, gram, gram_workspace_bytes,
+                   kron_factors, load, mlp_local_factors, sample_weights, solve, solve_antidiag,
                    status_string)

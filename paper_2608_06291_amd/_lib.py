@@ -17,7 +17,11 @@ BAKRON_OK, BAKRON_EINVAL, BAKRON_ENOTSPD, BAKRON_ENOMEM, BAKRON_EHIP = range(5)
 EXPORTED = ("bakron_factor", "bakron_solve", "bakron_solve_debug", "bakron_factors_free",
             "bakron_status_string", "bakron_factors_error", "bakron_last_error",
             "bakron_factor_export", "bakron_profile_enable", "bakron_profile_read",
-            "bakron_solve_check", "bakron_solve_antidiag")
+            "bakron_solve_check", "bakron_solve_antidiag", "bakron_gram",
+            "bakron_sample_weights", "bakron_kron_factors", "bakron_mlp_local_factors")
+
+BAKRON_KFAC, BAKRON_SHAMPOO = 0, 1
+STYLES = {"kfac": BAKRON_KFAC, "shampoo": BAKRON_SHAMPOO}
 
 _lib = None
 
@@ -77,6 +81,16 @@ def load(path: str = LIB_PATH):
                                           vp, vp]
     lib.bakron_solve_check.restype = ctypes.c_int
     lib.bakron_solve_check.argtypes = [vp, vp, ctypes.POINTER(ctypes.c_int32)]
+    i64, szp = ctypes.c_int64, ctypes.POINTER(ctypes.c_size_t)
+    lib.bakron_gram.restype = ctypes.c_int
+    lib.bakron_gram.argtypes = [vp, i64, i64, vp, ctypes.c_float, vp, vp, vp, szp, vp]
+    lib.bakron_sample_weights.restype = ctypes.c_int
+    lib.bakron_sample_weights.argtypes = [vp, i64, i64, vp, vp, vp]
+    lib.bakron_kron_factors.restype = ctypes.c_int
+    lib.bakron_kron_factors.argtypes = [vp, vp, i64, i64, i64, ctypes.c_int32, vp, vp, vp, szp, vp]
+    lib.bakron_mlp_local_factors.restype = ctypes.c_int
+    lib.bakron_mlp_local_factors.argtypes = [vp, vp, vp, i64, i64, i64, ctypes.c_int32, vp, vp, vp,
+                                             szp, vp]
     _lib = lib
     return lib
 
@@ -252,3 +266,122 @@ def solve_antidiag(W, f: Factors, bits: int, scale, codes=None, V=None, pre=None
     if st != BAKRON_OK:
         raise BakronError(st, f.error())
     return (codes, V) if pre is None else (codes, V, pre)
+
+
+# ---------------------------------------------------------------- factor construction
+def _ptr(t):
+    return ctypes.c_void_p(t.data_ptr() if t is not None else None)
+
+
+def _raise_last(st):
+    if st != BAKRON_OK:
+        raise BakronError(st, load().bakron_last_error().decode())
+
+
+def _with_workspace(call, device):
+    """Run a workspace-protocol entry point: query the size, allocate a torch
+    buffer (256-byte aligned by the caching allocator), then call."""
+    import torch
+    need = ctypes.c_size_t(0)
+    _raise_last(call(ctypes.c_void_p(None), ctypes.byref(need)))
+    work = torch.empty(max(int(need.value), 256), dtype=torch.uint8, device=device)
+    if work.data_ptr() % 256:
+        raise RuntimeError("workspace is not 256-byte aligned")
+    size = ctypes.c_size_t(work.numel())
+    _raise_last(call(_ptr(work), ctypes.byref(size)))
+    return work
+
+
+def gram(X, w=None, s: float = 1.0, M=None, C=None, work=None):
+    """bakron_gram: C = s * (X^T diag(w) X) (.) M on the current stream.
+    X: N x d fp32; w: N or None; M: d x d or None (may be C itself)."""
+    import torch
+    lib = load()
+    _check_dev(X, "X", torch.float32)
+    N, d = X.shape
+    for t, name, shape in ((w, "w", (N,)), (M, "M", (d, d))):
+        if t is not None:
+            _check_dev(t, name, torch.float32)
+            if tuple(t.shape) != shape:
+                raise ValueError(f"{name} must have shape {shape}")
+    if C is None:
+        C = torch.empty((d, d), dtype=torch.float32, device=X.device)
+    _check_dev(C, "C", torch.float32)
+    if tuple(C.shape) != (d, d):
+        raise ValueError("C must be d x d")
+    st = _stream(torch, X.device)
+
+    def call(wk, nbytes):
+        return lib.bakron_gram(_ptr(X), N, d, _ptr(w), float(s), _ptr(M), _ptr(C), wk, nbytes, st)
+    if work is None:
+        _with_workspace(call, X.device)
+    else:
+        size = ctypes.c_size_t(work.numel() * work.element_size())
+        _raise_last(call(_ptr(work), ctypes.byref(size)))
+    return C
+
+
+def gram_workspace_bytes(N: int, d: int) -> int:
+    """Workspace bytes bakron_gram needs for an N x d sample matrix on the
+    current device."""
+    need = ctypes.c_size_t(0)
+    _raise_last(load().bakron_gram(None, N, d, None, 1.0, None, None, None, ctypes.byref(need),
+                                   None))
+    return int(need.value)
+
+
+def sample_weights(X, c=None, w=None):
+    """bakron_sample_weights: w_k = sum_i c_i X_ki^2 on the current stream."""
+    import torch
+    lib = load()
+    _check_dev(X, "X", torch.float32)
+    N, d = X.shape
+    if c is not None:
+        _check_dev(c, "c", torch.float32)
+        if c.numel() != d:
+            raise ValueError("c must have d entries")
+    if w is None:
+        w = torch.empty((N,), dtype=torch.float32, device=X.device)
+    _check_dev(w, "w", torch.float32)
+    _raise_last(lib.bakron_sample_weights(_ptr(X), N, d, _ptr(c), _ptr(w),
+                                          _stream(torch, X.device)))
+    return w
+
+
+def kron_factors(a, b, style: str = "kfac"):
+    """bakron_kron_factors: (A, B) of a global Hessian from paired vector
+    samples a (N x n) and b (N x m) on the current stream."""
+    import torch
+    lib = load()
+    _check_dev(a, "a", torch.float32)
+    _check_dev(b, "b", torch.float32)
+    N, n = a.shape
+    if b.shape[0] != N:
+        raise ValueError("a and b need the same number of samples")
+    m = b.shape[1]
+    A = torch.empty((n, n), dtype=torch.float32, device=a.device)
+    B = torch.empty((m, m), dtype=torch.float32, device=a.device)
+    st = _stream(torch, a.device)
+    _with_workspace(lambda wk, nb: lib.bakron_kron_factors(_ptr(a), _ptr(b), N, n, m, STYLES[style],
+                                                           _ptr(A), _ptr(B), wk, nb, st), a.device)
+    return A, B
+
+
+def mlp_local_factors(x, g, D, style: str = "kfac"):
+    """bakron_mlp_local_factors: (A, B) of the MLP-local Hessian from inputs x
+    (N x dm), features g or f (N x dff) and W_down D (dm x dff)."""
+    import torch
+    lib = load()
+    for t, name in ((x, "x"), (g, "g"), (D, "D")):
+        _check_dev(t, name, torch.float32)
+    N, dm = x.shape
+    dff = g.shape[1]
+    if g.shape[0] != N or tuple(D.shape) != (dm, dff):
+        raise ValueError("shapes must be x: N x dm, g: N x dff, D: dm x dff")
+    A = torch.empty((dm, dm), dtype=torch.float32, device=x.device)
+    B = torch.empty((dff, dff), dtype=torch.float32, device=x.device)
+    st = _stream(torch, x.device)
+    _with_workspace(lambda wk, nb: lib.bakron_mlp_local_factors(_ptr(x), _ptr(g), _ptr(D), N, dm,
+                                                                dff, STYLES[style], _ptr(A),
+                                                                _ptr(B), wk, nb, st), x.device)
+    return A, B

@@ -4,7 +4,8 @@ import subprocess
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
-SOURCES = ["csrc/api.hip", "csrc/factor.hip", "csrc/solve.hip", "csrc/antidiag.hip"]
+SOURCES = ["csrc/api.hip", "csrc/factor.hip", "csrc/solve.hip", "csrc/antidiag.hip",
+           "csrc/hessian.hip"]
 LIB = os.path.join(HERE, "libbakron.so")
 
 HIPCC_FLAGS = [

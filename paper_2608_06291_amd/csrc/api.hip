@@ -82,6 +82,8 @@ extern "C" const char* bakron_status_string(bakron_status s) {
 
 extern "C" const char* bakron_last_error(void) { return g_last_error.c_str(); }
 
+void bk::set_last_error(const char* msg) { g_last_error = msg; }
+
 extern "C" const char* bakron_factors_error(const bakron_factors* f) {
     return f ? f->err.c_str() : "";
 }

@@ -95,4 +95,7 @@ constexpr int SEG_GRID = 256;
 // J0 of the MT x MT macro tile, z = (first source tile << 1) | push kind
 // (0 column push, 1 row push), w = end of the source tile range.
 
+// Records the message returned by bakron_last_error() for this thread.
+void set_last_error(const char* msg);
+
 }  // namespace bk

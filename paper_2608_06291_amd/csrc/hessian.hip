@@ -1,0 +1,453 @@
+// Kronecker-factor construction from calibration samples (Sec. 4 and App. A).
+// Every factor the paper forms is a weighted Gram matrix of per-sample vectors,
+// possibly multiplied entrywise by a fixed matrix:
+//     C = s * (X^T diag(w) X) (.) M,    C_ij = s * M_ij * sum_k w_k X_ki X_kj,
+// X the N x d matrix of samples (one row per sample):
+//   K-FAC style (App. A):         A = E[a a^T], B = E[b b^T]                  (w = 1, M = 1)
+//   single Shampoo step (App. A): A = E[|b|^2 a a^T], B = E[|a|^2 b b^T]      (w = squared norms)
+//   MLP-local (App. A, b = D_g W_down^T): b b^T = (g g^T) (.) W_down^T W_down, so
+//                                 B = E[g g^T] (.) D^T D with D^T D itself a Gram over the rows of
+//                                 D = W_down, and tr(b^T b) = sum_i (D^T D)_ii g_i^2.
+// k_sample_weights forms w_k = sum_i c_i X_ki^2 (c = 1: the squared norm).
+// k_gram computes the upper-triangle 128 x 128 blocks of X^T diag(w) X on fp32
+// MFMA, split over slices of the samples; k_gram_reduce adds the slices in a
+// fixed order, applies s and M, writes the upper triangle and mirrors it.
+#include <algorithm>
+#include <cstdio>
+#include <string>
+
+#include "bakron.h"
+#include "common.h"
+
+namespace bk {
+
+constexpr int GB = 128;        // Gram block edge
+constexpr int GK = 32;         // samples per chunk
+constexpr int GSTR = GK + 4;   // LDS row stride (floats) of a staged block
+
+// ----------------------------------------------------------------------------
+// w[k] = sum_i c[i] * X[k][i]^2 (c null: c = 1).  One wave per sample row.
+template <bool VEC>
+__global__ __launch_bounds__(256) void k_sample_weights(const float* __restrict__ X, int64_t N,
+                                                        int64_t d, const float* __restrict__ c,
+                                                        float* __restrict__ w) {
+    const int64_t k = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    const int l = threadIdx.x & 63;
+    if (k >= N) return;
+    const float* row = X + k * d;
+    float acc = 0.0f;
+    if (VEC) {
+        for (int64_t i = 4 * l; i < d; i += 256) {
+            const f32x4 x = *reinterpret_cast<const f32x4*>(row + i);
+            const f32x4 cc = c ? *reinterpret_cast<const f32x4*>(c + i) : f32x4{1.f, 1.f, 1.f, 1.f};
+#pragma unroll
+            for (int u = 0; u < 4; ++u) acc = fmaf(cc[u] * x[u], x[u], acc);
+        }
+    } else {
+        for (int64_t i = l; i < d; i += 64) {
+            const float x = row[i];
+            acc = fmaf(c ? c[i] * x : x, x, acc);
+        }
+    }
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) acc += __shfl_xor(acc, off);
+    if (l == 0) w[k] = acc;
+}
+
+// dst[i] = src[i * (d + 1)]: the diagonal of a d x d matrix.
+__global__ __launch_bounds__(256) void k_diag(const float* __restrict__ src, int64_t d,
+                                              float* __restrict__ dst) {
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i < d) dst[i] = src[i * (d + 1)];
+}
+
+// ----------------------------------------------------------------------------
+// Upper-triangle block (bi, bj), bi <= bj, of X^T diag(w) X over the samples of
+// one slice [k_lo, k_hi): part[slice][blk] (128 x 128, row-major).
+// A chunk is 32 samples.  Thread t stages features 4 (t & 31) .. + 3 of both
+// column ranges for samples 4 (t >> 5) .. + 3: four 16-byte row loads per
+// operand, transposed in registers, written as four 16-byte LDS rows
+// [feature][sample], so the MFMA operands below are contiguous along the
+// sample index (lane half h takes sample 16h + s at step s of
+// v_mfma_f32_32x32x2f32).  The first operand carries the weights.  4 waves,
+// each 2 x 2 MFMA blocks of 32 x 32; LDS double-buffered, the next chunk in
+// registers while the current one is multiplied.
+struct GramArgs {
+    const float* X;
+    int64_t N, d;
+    const float* w;
+    int64_t slice_rows;   // samples per slice, a multiple of GK
+    int nb, nblk;         // blocks per side, upper-triangle blocks
+    float* part;          // [slices][nblk][GB * GB]
+};
+
+__device__ inline void gram_block_of(int blk, int nb, int& bi, int& bj) {
+    int i = 0, rem = blk;   // row-major over the upper triangle
+    while (rem >= nb - i) {
+        rem -= nb - i;
+        ++i;
+    }
+    bi = i;
+    bj = i + rem;
+}
+
+template <bool VEC>
+__global__ __launch_bounds__(256, 2) void k_gram(GramArgs a) {
+    __shared__ __attribute__((aligned(16))) float As[2][GB][GSTR];
+    __shared__ __attribute__((aligned(16))) float Bs[2][GB][GSTR];
+    const int slice = (int)(blockIdx.x / (unsigned)a.nblk);
+    const int blk = (int)(blockIdx.x % (unsigned)a.nblk);
+    int bi, bj;
+    gram_block_of(blk, a.nb, bi, bj);
+    const int64_t i0 = (int64_t)bi * GB, j0 = (int64_t)bj * GB;
+    const int64_t k_lo = (int64_t)slice * a.slice_rows;
+    const int64_t k_hi = min(a.N, k_lo + a.slice_rows);
+    const int nch = k_hi > k_lo ? (int)((k_hi - k_lo + GK - 1) / GK) : 0;
+
+    const int tid = threadIdx.x;
+    const int wv = tid >> 6, l = tid & 63;
+    const int wm = wv >> 1, wn = wv & 1;
+    const int lr = l & 31, lk = l >> 5;
+    const int f4 = 4 * (tid & 31), kq = 4 * (tid >> 5);
+    const float* X = a.X;
+    const int64_t d = a.d;
+    f32x4 ra[4], rb[4];
+    auto load = [&](int64_t k0) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int64_t k = k0 + kq + r;
+            const bool kin = k < k_hi;
+            const float wk = kin ? (a.w ? a.w[k] : 1.0f) : 0.0f;
+            const float* row = X + (kin ? k : 0) * d;
+            if (VEC) {
+                const f32x4 z = {0.f, 0.f, 0.f, 0.f};
+                ra[r] = (kin && i0 + f4 < d) ? *reinterpret_cast<const f32x4*>(row + i0 + f4) * wk : z;
+                rb[r] = (kin && j0 + f4 < d) ? *reinterpret_cast<const f32x4*>(row + j0 + f4) : z;
+            } else {
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    ra[r][u] = (kin && i0 + f4 + u < d) ? row[i0 + f4 + u] * wk : 0.0f;
+                    rb[r][u] = (kin && j0 + f4 + u < d) ? row[j0 + f4 + u] : 0.0f;
+                }
+            }
+        }
+    };
+    auto store = [&](int sb) {
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            *reinterpret_cast<f32x4*>(&As[sb][f4 + u][kq]) = f32x4{ra[0][u], ra[1][u], ra[2][u], ra[3][u]};
+            *reinterpret_cast<f32x4*>(&Bs[sb][f4 + u][kq]) = f32x4{rb[0][u], rb[1][u], rb[2][u], rb[3][u]};
+        }
+    };
+    f32x16 acc[2][2];
+#pragma unroll
+    for (int x = 0; x < 2; ++x)
+#pragma unroll
+        for (int y = 0; y < 2; ++y) acc[x][y] = f32x16{0};
+    if (nch > 0) {
+        load(k_lo);
+        store(0);
+    }
+    __syncthreads();
+    for (int c = 0; c < nch; ++c) {
+        const int sb = c & 1;
+        const bool more = c + 1 < nch;
+        if (more) load(k_lo + (int64_t)(c + 1) * GK);
+        f32x4 fa[2][4], fb[2][4];
+#pragma unroll
+        for (int x = 0; x < 2; ++x)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                fa[x][v] = *reinterpret_cast<const f32x4*>(&As[sb][(2 * wm + x) * TS + lr][lk * 16 + v * 4]);
+                fb[x][v] = *reinterpret_cast<const f32x4*>(&Bs[sb][(2 * wn + x) * TS + lr][lk * 16 + v * 4]);
+            }
+#pragma unroll
+        for (int st = 0; st < 16; ++st)
+#pragma unroll
+            for (int x = 0; x < 2; ++x)
+#pragma unroll
+                for (int y = 0; y < 2; ++y)
+                    acc[x][y] = __builtin_amdgcn_mfma_f32_32x32x2f32(fa[x][st >> 2][st & 3],
+                                                                    fb[y][st >> 2][st & 3], acc[x][y],
+                                                                    0, 0, 0);
+        if (more) store(sb ^ 1);
+        __syncthreads();
+    }
+    // acc[x][y][r] is entry (row (2wm + x) * 32 + (r >> 2) * 8 + lk * 4 + (r & 3),
+    // column (2wn + y) * 32 + lr) of the block
+    float* P = a.part + ((int64_t)slice * a.nblk + blk) * (GB * GB);
+#pragma unroll
+    for (int x = 0; x < 2; ++x)
+#pragma unroll
+        for (int y = 0; y < 2; ++y)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int row = (2 * wm + x) * TS + (r >> 2) * 8 + lk * 4 + (r & 3);
+                P[row * GB + (2 * wn + y) * TS + lr] = acc[x][y][r];
+            }
+}
+
+// One 32 x 32 sub-tile of a block: sum the slices in order and scale; write
+// the upper-triangle entries, C[i][j] = s * G_ij * M_ij (i <= j), and mirror
+// them, C[j][i] = s * G_ij * M_ji (i < j), so that C is exactly symmetric when
+// M is (the weighted products of a diagonal block are not bitwise symmetric).
+// Sub-tiles below the diagonal of a diagonal block are skipped: their entries
+// are the mirror of the sub-tile above.  Every entry of C is read (M) and
+// written by one thread, so M may alias C.
+__global__ __launch_bounds__(256) void k_gram_reduce(const float* __restrict__ part, int slices,
+                                                     int nblk, int nb, int64_t d, float s,
+                                                     const float* M, float* C) {
+    __shared__ float T[TS][TS + 1];
+    const int blk = (int)(blockIdx.x >> 4), sub = (int)(blockIdx.x & 15);
+    int bi, bj;
+    gram_block_of(blk, nb, bi, bj);
+    const int sr = sub >> 2, sc = sub & 3;
+    if (bi == bj && sr > sc) return;
+    const bool diag = bi == bj && sr == sc;   // the sub-tile straddles the diagonal
+    const int r = threadIdx.x >> 3, c4 = 4 * (threadIdx.x & 7);
+    const int64_t bo = (int64_t)blk * (GB * GB) + (sr * TS + r) * GB + sc * TS + c4;
+    f32x4 g = {0.f, 0.f, 0.f, 0.f};
+    for (int sl = 0; sl < slices; ++sl)
+        g += *reinterpret_cast<const f32x4*>(part + (int64_t)sl * nblk * (GB * GB) + bo);
+    g *= s;
+    const int64_t i = (int64_t)bi * GB + sr * TS + r;
+    const int64_t jb = (int64_t)bj * GB + sc * TS + c4;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+        if (i < d && jb + u < d && (!diag || r <= c4 + u)) {
+            const int64_t o = i * d + jb + u;
+            C[o] = M ? g[u] * M[o] : g[u];
+        }
+        T[r][c4 + u] = g[u];
+    }
+    __syncthreads();
+    const int64_t il = (int64_t)bj * GB + sc * TS + r;   // mirrored row
+    const int64_t jl = (int64_t)bi * GB + sr * TS + c4;  // mirrored columns
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+        if (il < d && jl + u < d && (!diag || r > c4 + u)) {
+            const int64_t o = il * d + jl + u;
+            const float v = T[c4 + u][r];
+            C[o] = M ? v * M[o] : v;
+        }
+    }
+}
+
+// ----------------------------------------------------------------------------
+// Launch geometry of one Gram product.  The blocks of one slice are
+// consecutive workgroups (they stream the same samples, which stay in L2);
+// the slice count balances nblk * slices blocks over the 2 * ncu workgroup
+// slots (two workgroups fit one CU), charging each slice its partial-sum
+// traffic.
+struct GramGeom {
+    int nb, nblk, slices;
+    int64_t slice_rows;
+};
+
+static GramGeom gram_geom(int64_t N, int64_t d, int ncu) {
+    GramGeom g;
+    g.nb = (int)((d + GB - 1) / GB);
+    g.nblk = g.nb * (g.nb + 1) / 2;
+    const int64_t nch = std::max<int64_t>(1, (N + GK - 1) / GK);
+    const int64_t slots = 2 * (int64_t)std::max(ncu, 1);
+    int best = 1;
+    double best_t = 0.0;
+    for (int S = 1; S <= 64 && S <= nch; ++S) {
+        const int64_t per = (nch + S - 1) / S;
+        const int64_t S_eff = (nch + per - 1) / per;
+        // in chunk-times of one workgroup (2 * 128 * 128 * 32 flops at half a
+        // CU's MFMA rate, about 3.4 us): the waves of blocks, plus writing and
+        // reading back every 64 KiB partial at about 5 TB/s (0.0077 each)
+        const double t = (double)((g.nblk * S_eff + slots - 1) / slots) * (double)per +
+                         0.0077 * (double)(g.nblk * S_eff);
+        if (S == 1 || t < best_t - 1e-9) {
+            best_t = t;
+            best = (int)S_eff;
+        }
+    }
+    const int64_t per = (nch + best - 1) / best;
+    g.slice_rows = per * GK;
+    g.slices = (int)((nch + per - 1) / per);
+    return g;
+}
+
+static size_t gram_part_bytes(const GramGeom& g) {
+    return (size_t)g.slices * g.nblk * GB * GB * sizeof(float);
+}
+
+static hipError_t run_sample_weights(hipStream_t st, const float* X, int64_t N, int64_t d,
+                                     const float* c, float* w) {
+    if (N == 0) return hipSuccess;
+    const bool vec = d % 4 == 0 && ((uintptr_t)X & 15) == 0 && (!c || ((uintptr_t)c & 15) == 0);
+    const dim3 grid((unsigned)((N + 3) / 4));
+    if (vec)
+        hipLaunchKernelGGL(k_sample_weights<true>, grid, dim3(256), 0, st, X, N, d, c, w);
+    else
+        hipLaunchKernelGGL(k_sample_weights<false>, grid, dim3(256), 0, st, X, N, d, c, w);
+    return hipGetLastError();
+}
+
+static hipError_t run_gram(hipStream_t st, const GramGeom& g, const float* X, int64_t N, int64_t d,
+                           const float* w, float s, const float* M, float* C, float* part) {
+    if (d == 0) return hipSuccess;
+    GramArgs a{X, N, d, w, g.slice_rows, g.nb, g.nblk, part};
+    const bool vec = d % 4 == 0 && ((uintptr_t)X & 15) == 0;
+    const dim3 grid((unsigned)((int64_t)g.nblk * g.slices));
+    if (vec)
+        hipLaunchKernelGGL(k_gram<true>, grid, dim3(256), 0, st, a);
+    else
+        hipLaunchKernelGGL(k_gram<false>, grid, dim3(256), 0, st, a);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k_gram_reduce, dim3((unsigned)(g.nblk * 16)), dim3(256), 0, st, part,
+                       g.slices, g.nblk, g.nb, d, s, M, C);
+    return hipGetLastError();
+}
+
+static int device_cus() {
+    int dev = 0, ncu = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return 0;
+    if (hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+    return ncu;
+}
+
+}  // namespace bk
+
+// ============================================================================
+// C ABI (declared in bakron.h)
+
+using bk::GramGeom;
+
+static bakron_status hess_fail(const char* msg) {
+    bk::set_last_error(msg);
+    return BAKRON_EINVAL;
+}
+
+static bakron_status hess_hip(hipError_t e, const char* what) {
+    char buf[256];
+    std::snprintf(buf, sizeof(buf), "%s: %s", what, hipGetErrorString(e));
+    bk::set_last_error(buf);
+    return e == hipErrorOutOfMemory ? BAKRON_ENOMEM : BAKRON_EHIP;
+}
+
+static inline size_t align256(size_t b) { return (b + 255) & ~(size_t)255; }
+
+// Dimension limits: blocks per side fit the launch grid comfortably.
+static const int64_t HESS_DIM_MAX = (int64_t)1 << 17;
+static const int64_t HESS_N_MAX = (int64_t)1 << 40;
+
+// Workspace handshake shared by the factor-construction calls: with work ==
+// NULL report the size; otherwise check it.
+static bakron_status workspace_check(void* work, size_t* work_bytes, size_t need, bool* query) {
+    *query = false;
+    if (!work_bytes) return hess_fail("work_bytes is NULL");
+    if (!work) {
+        *work_bytes = need;
+        *query = true;
+        return BAKRON_OK;
+    }
+    if (*work_bytes < need) return hess_fail("workspace too small");
+    if (((uintptr_t)work & 255) != 0) return hess_fail("workspace not 256-byte aligned");
+    return BAKRON_OK;
+}
+
+extern "C" bakron_status bakron_sample_weights(const float* X, int64_t N, int64_t d, const float* c,
+                                               float* w, hipStream_t stream) {
+    bk::set_last_error("");
+    if (N < 0 || d < 0 || N > HESS_N_MAX || d > HESS_DIM_MAX) return hess_fail("bad size");
+    if (N > 0 && (!w || (d > 0 && !X))) return hess_fail("null pointer");
+    hipError_t e = bk::run_sample_weights(stream, X, N, d, c, w);
+    return e == hipSuccess ? BAKRON_OK : hess_hip(e, "bakron_sample_weights: launch");
+}
+
+extern "C" bakron_status bakron_gram(const float* X, int64_t N, int64_t d, const float* w, float s,
+                                     const float* M, float* C, void* work, size_t* work_bytes,
+                                     hipStream_t stream) {
+    bk::set_last_error("");
+    if (N < 0 || d < 0 || N > HESS_N_MAX || d > HESS_DIM_MAX) return hess_fail("bad size");
+    const GramGeom g = bk::gram_geom(N, d, bk::device_cus());
+    bool query;
+    bakron_status st = workspace_check(work, work_bytes, bk::gram_part_bytes(g), &query);
+    if (st != BAKRON_OK || query) return st;
+    if (d > 0 && (!C || (N > 0 && !X))) return hess_fail("null pointer");
+    hipError_t e = bk::run_gram(stream, g, X, N, d, w, s, M, C, static_cast<float*>(work));
+    return e == hipSuccess ? BAKRON_OK : hess_hip(e, "bakron_gram: launch");
+}
+
+extern "C" bakron_status bakron_kron_factors(const float* a, const float* b, int64_t N, int64_t n,
+                                             int64_t m, int32_t style, float* A, float* B,
+                                             void* work, size_t* work_bytes, hipStream_t stream) {
+    bk::set_last_error("");
+    if (N <= 0 || n <= 0 || m <= 0 || N > HESS_N_MAX || n > HESS_DIM_MAX || m > HESS_DIM_MAX)
+        return hess_fail("bad size");
+    if (style != BAKRON_KFAC && style != BAKRON_SHAMPOO) return hess_fail("bad style");
+    const int ncu = bk::device_cus();
+    const GramGeom ga = bk::gram_geom(N, n, ncu), gb = bk::gram_geom(N, m, ncu);
+    const size_t part = std::max(bk::gram_part_bytes(ga), bk::gram_part_bytes(gb));
+    const size_t wbytes = style == BAKRON_SHAMPOO ? align256((size_t)N * sizeof(float)) : 0;
+    bool query;
+    bakron_status st = workspace_check(work, work_bytes, align256(part) + 2 * wbytes, &query);
+    if (st != BAKRON_OK || query) return st;
+    if (!a || !b || !A || !B) return hess_fail("null pointer");
+    float* P = static_cast<float*>(work);
+    float* wa = nullptr;   // |a_k|^2, weights of B
+    float* wb = nullptr;   // |b_k|^2, weights of A
+    const float inv = (float)(1.0 / (double)N);
+    hipError_t e = hipSuccess;
+    if (style == BAKRON_SHAMPOO) {
+        wa = reinterpret_cast<float*>(static_cast<char*>(work) + align256(part));
+        wb = reinterpret_cast<float*>(reinterpret_cast<char*>(wa) + wbytes);
+        if ((e = bk::run_sample_weights(stream, a, N, n, nullptr, wa)) != hipSuccess ||
+            (e = bk::run_sample_weights(stream, b, N, m, nullptr, wb)) != hipSuccess)
+            return hess_hip(e, "bakron_kron_factors: weights");
+    }
+    if ((e = bk::run_gram(stream, ga, a, N, n, wb, inv, nullptr, A, P)) != hipSuccess ||
+        (e = bk::run_gram(stream, gb, b, N, m, wa, inv, nullptr, B, P)) != hipSuccess)
+        return hess_hip(e, "bakron_kron_factors: gram");
+    return BAKRON_OK;
+}
+
+extern "C" bakron_status bakron_mlp_local_factors(const float* x, const float* g, const float* D,
+                                                  int64_t N, int64_t dm, int64_t dff, int32_t style,
+                                                  float* A, float* B, void* work, size_t* work_bytes,
+                                                  hipStream_t stream) {
+    bk::set_last_error("");
+    if (N <= 0 || dm <= 0 || dff <= 0 || N > HESS_N_MAX || dm > HESS_DIM_MAX || dff > HESS_DIM_MAX)
+        return hess_fail("bad size");
+    if (style != BAKRON_KFAC && style != BAKRON_SHAMPOO) return hess_fail("bad style");
+    const int ncu = bk::device_cus();
+    const GramGeom gx = bk::gram_geom(N, dm, ncu), gg = bk::gram_geom(N, dff, ncu),
+                   gd = bk::gram_geom(dm, dff, ncu);
+    const size_t part = std::max({bk::gram_part_bytes(gx), bk::gram_part_bytes(gg),
+                                  bk::gram_part_bytes(gd)});
+    const size_t wbytes = style == BAKRON_SHAMPOO ? align256((size_t)N * sizeof(float)) : 0;
+    const size_t cbytes = style == BAKRON_SHAMPOO ? align256((size_t)dff * sizeof(float)) : 0;
+    bool query;
+    bakron_status st = workspace_check(work, work_bytes, align256(part) + 2 * wbytes + cbytes, &query);
+    if (st != BAKRON_OK || query) return st;
+    if (!x || !g || !D || !A || !B) return hess_fail("null pointer");
+    float* P = static_cast<float*>(work);
+    const float inv = (float)(1.0 / (double)N);
+    hipError_t e;
+    // D^T D (rows of D = W_down as samples) into B
+    if ((e = bk::run_gram(stream, gd, D, dm, dff, nullptr, 1.0f, nullptr, B, P)) != hipSuccess)
+        return hess_hip(e, "bakron_mlp_local_factors: D^T D");
+    float* wx = nullptr;   // |x_k|^2, weights of B
+    float* wg = nullptr;   // g_k^T diag(D^T D) g_k = tr(b_k^T b_k), weights of A
+    if (style == BAKRON_SHAMPOO) {
+        wx = reinterpret_cast<float*>(static_cast<char*>(work) + align256(part));
+        wg = reinterpret_cast<float*>(reinterpret_cast<char*>(wx) + wbytes);
+        float* cdiag = reinterpret_cast<float*>(reinterpret_cast<char*>(wg) + wbytes);
+        hipLaunchKernelGGL(bk::k_diag, dim3((unsigned)((dff + 255) / 256)), dim3(256), 0, stream, B,
+                           dff, cdiag);
+        if ((e = hipGetLastError()) != hipSuccess ||
+            (e = bk::run_sample_weights(stream, g, N, dff, cdiag, wg)) != hipSuccess ||
+            (e = bk::run_sample_weights(stream, x, N, dm, nullptr, wx)) != hipSuccess)
+            return hess_hip(e, "bakron_mlp_local_factors: weights");
+    }
+    // A = E[w_g x x^T]; B = E[w_x g g^T] (.) D^T D, in place over D^T D
+    if ((e = bk::run_gram(stream, gx, x, N, dm, wg, inv, nullptr, A, P)) != hipSuccess ||
+        (e = bk::run_gram(stream, gg, g, N, dff, wx, inv, B, B, P)) != hipSuccess)
+        return hess_hip(e, "bakron_mlp_local_factors: gram");
+    return BAKRON_OK;
+}

@@ -71,3 +71,52 @@ def test_binding_refuses_cpu_tensors():
     import paper_2608_06291_amd as pk
     with pytest.raises(TypeError):
         pk.factor(torch.eye(4), None, 0.01)
+
+
+def test_factor_construction_host_validation(lib):
+    """The factor-construction calls answer workspace queries and reject bad
+    arguments on the host, before any HIP call."""
+    import paper_2608_06291_amd as pk
+    one = ctypes.c_void_p(256)
+    need = ctypes.c_size_t(0)
+    # workspace query: size only, pointers unchecked; grows with the problem
+    assert lib.bakron_gram(None, 1000, 200, None, 1.0, None, None, None,
+                           ctypes.byref(need), None) == pk.BAKRON_OK
+    small = need.value
+    assert small > 0 and small % 256 == 0
+    assert lib.bakron_gram(None, 100000, 1000, None, 1.0, None, None, None,
+                           ctypes.byref(need), None) == pk.BAKRON_OK
+    assert need.value > small
+    # too small, unaligned, missing size, bad sizes
+    need = ctypes.c_size_t(16)
+    assert lib.bakron_gram(one, 1000, 200, None, 1.0, None, one, one, ctypes.byref(need),
+                           None) == pk.BAKRON_EINVAL
+    assert b"too small" in lib.bakron_last_error()
+    need = ctypes.c_size_t(1 << 30)
+    assert lib.bakron_gram(one, 1000, 200, None, 1.0, None, one, ctypes.c_void_p(258),
+                           ctypes.byref(need), None) == pk.BAKRON_EINVAL
+    assert lib.bakron_gram(one, 10, 20, None, 1.0, None, one, one, None, None) == pk.BAKRON_EINVAL
+    assert lib.bakron_gram(one, -1, 20, None, 1.0, None, one, None, ctypes.byref(need),
+                           None) == pk.BAKRON_EINVAL
+    assert lib.bakron_gram(one, 10, (1 << 17) + 1, None, 1.0, None, one, None,
+                           ctypes.byref(need), None) == pk.BAKRON_EINVAL
+    assert lib.bakron_gram(None, 10, 20, None, 1.0, None, one, one, ctypes.byref(need),
+                           None) == pk.BAKRON_EINVAL
+    # composite calls: bad style, N = 0, shampoo needs more workspace than K-FAC
+    for fn, args in ((lib.bakron_kron_factors, (one, one, 64, 32, 48)),
+                     (lib.bakron_mlp_local_factors, (one, one, one, 64, 32, 48))):
+        q = ctypes.c_size_t(0)
+        assert fn(*args, 7, one, one, None, ctypes.byref(q), None) == pk.BAKRON_EINVAL
+        assert b"style" in lib.bakron_last_error()
+        bad = list(args)
+        bad[-3] = 0
+        assert fn(*bad, pk.BAKRON_KFAC, one, one, None, ctypes.byref(q), None) == pk.BAKRON_EINVAL
+        assert fn(*args, pk.BAKRON_KFAC, one, one, None, ctypes.byref(q), None) == pk.BAKRON_OK
+        kfac = q.value
+        assert fn(*args, pk.BAKRON_SHAMPOO, one, one, None, ctypes.byref(q), None) == pk.BAKRON_OK
+        assert q.value > kfac
+        q = ctypes.c_size_t(q.value)
+        assert fn(*args, pk.BAKRON_SHAMPOO, None, one, one, ctypes.byref(q),
+                  None) == pk.BAKRON_EINVAL
+    assert lib.bakron_sample_weights(None, 10, 4, None, one, None) == pk.BAKRON_EINVAL
+    assert lib.bakron_sample_weights(one, -2, 4, None, one, None) == pk.BAKRON_EINVAL
