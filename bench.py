@@ -176,7 +176,8 @@ def _gram_flops(N: int, d: int) -> float:
     return float(N) * d * (d + 1)
 
 
-def factors_bench(steps: int, warmup: int, n_samples: int, cpu_seconds: float, do_cpu: bool):
+def factors_bench(steps: int, warmup: int, n_samples: int, cpu_seconds: float, do_cpu: bool,
+                  only: str | None = None):
     """One JSON line per Kronecker-factor workload: the whole factor
     construction per step (every Gram, weight and mask of the pair), the
     dominant Gram launch timed alone for the roofline, 48 entries of each
@@ -191,7 +192,11 @@ def factors_bench(steps: int, warmup: int, n_samples: int, cpu_seconds: float, d
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     N = n_samples
     cache = {}
-    for name, style in FACTOR_WORKLOADS:
+    todo = [w for w in FACTOR_WORKLOADS if only is None or ":".join(w) == only]
+    if not todo:
+        raise SystemExit(f"unknown --factor-only {only}; one of "
+                         + ", ".join(":".join(w) for w in FACTOR_WORKLOADS))
+    for name, style in todo:
         if name not in cache:
             cache.clear()
             torch.cuda.empty_cache()
@@ -362,6 +367,8 @@ def main():
     ap.add_argument("--factors", action="store_true",
                     help="only run the Kronecker-factor construction workloads (App. A: K-FAC and "
                          "single-step Shampoo, global and MLP-local) and exit; one JSON line each")
+    ap.add_argument("--factor-only", default=None,
+                    help="with --factors: run only this workload:style (e.g. global-4096x4096:kfac)")
     ap.add_argument("--factor-samples", type=int, default=FACTOR_N,
                     help="calibration samples for --factors (default 256 x 2048)")
     args = ap.parse_args()
@@ -380,7 +387,7 @@ def main():
 
     if args.factors:
         factors_bench(args.steps, args.warmup, args.factor_samples, args.cpu_seconds,
-                      not args.no_cpu_baseline)
+                      not args.no_cpu_baseline, args.factor_only)
         return
 
     if args.copy_calibration_mib > 0:

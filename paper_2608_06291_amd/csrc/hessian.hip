@@ -111,28 +111,47 @@ __global__ __launch_bounds__(256, 2) void k_gram(GramArgs a) {
     const int f4 = 4 * (tid & 31), kq = 4 * (tid >> 5);
     const float* X = a.X;
     const int64_t d = a.d;
+    // Loads are unconditional, from clamped (always valid) addresses, so that
+    // they stay in flight across the MFMAs of the current chunk; the weights
+    // and the masks of rows past the slice and columns past d are applied when
+    // the registers are written to LDS.
+    const bool a_in = i0 + f4 < d, b_in = j0 + f4 < d;
+    const int64_t ia = a_in ? i0 + f4 : 0, ja = b_in ? j0 + f4 : 0;
     f32x4 ra[4], rb[4];
+    float rw[4];
+    int64_t kbase = 0;
     auto load = [&](int64_t k0) {
+        kbase = k0;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-            const int64_t k = k0 + kq + r;
-            const bool kin = k < k_hi;
-            const float wk = kin ? (a.w ? a.w[k] : 1.0f) : 0.0f;
-            const float* row = X + (kin ? k : 0) * d;
+            const int64_t k = min(k0 + kq + r, k_hi - 1);
+            const float* row = X + k * d;
+            rw[r] = a.w ? a.w[k] : 1.0f;
             if (VEC) {
-                const f32x4 z = {0.f, 0.f, 0.f, 0.f};
-                ra[r] = (kin && i0 + f4 < d) ? *reinterpret_cast<const f32x4*>(row + i0 + f4) * wk : z;
-                rb[r] = (kin && j0 + f4 < d) ? *reinterpret_cast<const f32x4*>(row + j0 + f4) : z;
+                ra[r] = *reinterpret_cast<const f32x4*>(row + ia);
+                rb[r] = *reinterpret_cast<const f32x4*>(row + ja);
             } else {
 #pragma unroll
                 for (int u = 0; u < 4; ++u) {
-                    ra[r][u] = (kin && i0 + f4 + u < d) ? row[i0 + f4 + u] * wk : 0.0f;
-                    rb[r][u] = (kin && j0 + f4 + u < d) ? row[j0 + f4 + u] : 0.0f;
+                    ra[r][u] = row[i0 + f4 + u < d ? i0 + f4 + u : 0];
+                    rb[r][u] = row[j0 + f4 + u < d ? j0 + f4 + u : 0];
                 }
             }
         }
     };
     auto store = [&](int sb) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const bool kin = kbase + kq + r < k_hi;
+            const float wk = kin ? rw[r] : 0.0f;
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const bool ca = VEC ? a_in : i0 + f4 + u < d;
+                const bool cb = VEC ? b_in : j0 + f4 + u < d;
+                ra[r][u] = ca ? ra[r][u] * wk : 0.0f;
+                rb[r][u] = (cb && kin) ? rb[r][u] : 0.0f;
+            }
+        }
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
             *reinterpret_cast<f32x4*>(&As[sb][f4 + u][kq]) = f32x4{ra[0][u], ra[1][u], ra[2][u], ra[3][u]};

@@ -179,18 +179,22 @@ def ar1_samples_torch(N: int, d: int, rho: float, gen, device, spike_rank: int =
     in fp32 (for full-size workloads; different random numbers from the numpy
     version).  Returns an N x d contiguous fp32 tensor."""
     import torch
-    eps = torch.randn((d, N), generator=gen, device=device)
+    # the recursion x_0 = e_0, x_t = rho x_{t-1} + c e_t unrolled: x = L e with
+    # L[t][s] = rho^(t-s) * (1 if s == 0 else c), one product for all samples
     c = float(np.sqrt(1.0 - rho * rho))
-    for t in range(1, d):   # feature-major rows: the recursion along the feature index
-        eps[t].mul_(c).add_(eps[t - 1], alpha=rho)
+    t = torch.arange(d, device=device, dtype=torch.float64)
+    L = torch.where(t[:, None] >= t[None, :], rho ** (t[:, None] - t[None, :]).clamp(min=0),
+                    torch.zeros((), dtype=torch.float64, device=device))
+    L[:, 1:] *= c
+    eps = torch.randn((N, d), generator=gen, device=device)
+    X = eps @ L.t().to(torch.float32)
+    del eps
     if spike_rank > 0:
         q, _ = torch.linalg.qr(torch.randn((d, spike_rank), generator=gen, device=device))
-        eps.addmm_(q, torch.randn((spike_rank, N), generator=gen, device=device) * np.sqrt(10.0))
+        X.addmm_(torch.randn((N, spike_rank), generator=gen, device=device) * np.sqrt(10.0), q.t())
     if norm_sigma > 0:
-        eps.mul_(torch.exp(norm_sigma * torch.randn((1, N), generator=gen, device=device)))
-    X = eps.t().contiguous()
-    del eps
-    return X
+        X.mul_(torch.exp(norm_sigma * torch.randn((N, 1), generator=gen, device=device)))
+    return X.contiguous()
 
 
 def kron_samples_torch(N: int, n: int, m: int, seed: int, device) -> dict:
