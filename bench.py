@@ -83,7 +83,7 @@ def cpu_baseline(cfg_inputs, seconds: float) -> dict:
                 host_nproc=os.cpu_count())
 
 
-def measured_traffic(kernel: str, workload: str):
+def measured_traffic(kernel: str, workload: str, sources=("solve.hip", "common.h")):
     """HBM bytes per launch from the committed rocprofv3 FETCH_SIZE/WRITE_SIZE
     summary, or None if there is none for this kernel and workload or the
     kernel sources changed since it was measured."""
@@ -93,7 +93,7 @@ def measured_traffic(kernel: str, workload: str):
         return None
     rec = json.load(open(path))
     src = b"".join(open(os.path.join(ROOT, "paper_2608_06291_amd", "csrc", f), "rb").read()
-                   for f in ("solve.hip", "common.h"))
+                   for f in sources)
     if hashlib.sha256(src).hexdigest() != rec.get("source_sha256"):
         return None
     return rec["bytes_per_launch"]
@@ -300,7 +300,9 @@ def factors_bench(steps: int, warmup: int, n_samples: int, cpu_seconds: float, d
                        "algorithmic_flops": F, "sampled_max_rel_err": rel},
             "roofline": {"kernel": "k_gram + k_gram_reduce (Gram of the N x %d operand)" % m,
                          "bound": "mfma", "achieved": g_tf, "peak": PEAK_FP32_MFMA,
-                         "unit": "TFLOP/s", "frac": g_tf / PEAK_FP32_MFMA, "traffic": None,
+                         "unit": "TFLOP/s", "frac": g_tf / PEAK_FP32_MFMA,
+                         "traffic": measured_traffic("k_gram", f"{name}-{style}",
+                                                     ("hessian.hip", "common.h")),
                          "launch_ms": g_ms},
             "cpu_baseline": cpu,
         }

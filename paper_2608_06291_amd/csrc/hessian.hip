@@ -78,25 +78,66 @@ struct GramArgs {
     const float* w;
     int64_t slice_rows;   // samples per slice, a multiple of GK
     int nb, nblk;         // blocks per side, upper-triangle blocks
+    int slices;
     float* part;          // [slices][nblk][GB * GB]
 };
 
-__device__ inline void gram_block_of(int blk, int nb, int& bi, int& bj) {
-    int i = 0, rem = blk;   // row-major over the upper triangle
-    while (rem >= nb - i) {
-        rem -= nb - i;
-        ++i;
+// Block t of a slice -> (bi, bj), bi <= bj.  The upper triangle is walked in
+// 8 x 8 supertiles (row-major over supertiles, row-major inside each), so that
+// consecutive blocks share few column ranges of X.
+constexpr int GSUPER = 8;
+__device__ inline void gram_block_of(int t, int nb, int& bi, int& bj) {
+    const int nS = (nb + GSUPER - 1) / GSUPER;
+    for (int SI = 0; SI < nS; ++SI) {
+        const int r0 = SI * GSUPER, r1 = min(nb, r0 + GSUPER);
+        for (int SJ = SI; SJ < nS; ++SJ) {
+            const int c0 = SJ * GSUPER, c1 = min(nb, c0 + GSUPER);
+            if (SI == SJ) {
+                const int w = r1 - r0;
+                if (t < w * (w + 1) / 2) {
+                    int i = r0;
+                    while (t >= r1 - i) {
+                        t -= r1 - i;
+                        ++i;
+                    }
+                    bi = i;
+                    bj = i + t;
+                    return;
+                }
+                t -= w * (w + 1) / 2;
+            } else {
+                const int cnt = (r1 - r0) * (c1 - c0);
+                if (t < cnt) {
+                    bi = r0 + t / (c1 - c0);
+                    bj = c0 + t % (c1 - c0);
+                    return;
+                }
+                t -= cnt;
+            }
+        }
     }
-    bi = i;
-    bj = i + rem;
+    bi = bj = 0;   // not reached for t < nb (nb + 1) / 2
+}
+
+// Work item of a k_gram workgroup.  Workgroups are dealt to the 8 XCDs in
+// turn (workgroup v runs on XCD v mod 8), so XCD x is given the contiguous
+// range x * per .. of the work list (slices in order, blocks of a slice in
+// supertile order): the workgroups resident on one XCD then stream the same
+// samples and few column ranges, which stay in that XCD's L2.
+constexpr int GXCD = 8;
+__device__ inline int gram_work_of(int v, int total) {
+    const int per = (total + GXCD - 1) / GXCD;
+    return (v % GXCD) * per + v / GXCD;
 }
 
 template <bool VEC>
 __global__ __launch_bounds__(256, 2) void k_gram(GramArgs a) {
     __shared__ __attribute__((aligned(16))) float As[2][GB][GSTR];
     __shared__ __attribute__((aligned(16))) float Bs[2][GB][GSTR];
-    const int slice = (int)(blockIdx.x / (unsigned)a.nblk);
-    const int blk = (int)(blockIdx.x % (unsigned)a.nblk);
+    const int wk = gram_work_of((int)blockIdx.x, a.nblk * a.slices);
+    if (wk >= a.nblk * a.slices) return;   // padding of the last XCD's range
+    const int slice = wk / a.nblk;
+    const int blk = wk % a.nblk;
     int bi, bj;
     gram_block_of(blk, a.nb, bi, bj);
     const int64_t i0 = (int64_t)bi * GB, j0 = (int64_t)bj * GB;
@@ -309,9 +350,10 @@ static hipError_t run_sample_weights(hipStream_t st, const float* X, int64_t N, 
 static hipError_t run_gram(hipStream_t st, const GramGeom& g, const float* X, int64_t N, int64_t d,
                            const float* w, float s, const float* M, float* C, float* part) {
     if (d == 0) return hipSuccess;
-    GramArgs a{X, N, d, w, g.slice_rows, g.nb, g.nblk, part};
+    GramArgs a{X, N, d, w, g.slice_rows, g.nb, g.nblk, g.slices, part};
     const bool vec = d % 4 == 0 && ((uintptr_t)X & 15) == 0;
-    const dim3 grid((unsigned)((int64_t)g.nblk * g.slices));
+    const int64_t total = (int64_t)g.nblk * g.slices;
+    const dim3 grid((unsigned)(((total + GXCD - 1) / GXCD) * GXCD));
     if (vec)
         hipLaunchKernelGGL(k_gram<true>, grid, dim3(256), 0, st, a);
     else
