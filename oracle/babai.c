@@ -17,41 +17,44 @@
  *   Python side of the oracle forms them.
  *
  * "round" is replaced by "quantise to the nearest alphabet element"
- * (Sec. 3.1): symmetric alphabet {-l..l}, per-row scale s_i (App. D), i.e.
- *   c = clamp(rint(x), -l, l),   x = W~_ij / s_i,   v = s_i * c.
+ * (Sec. 3.1): an alphabet of consecutive integers {lo..hi} (symmetric
+ * {-l..l} as in App. D, or the (b+1)-bit {-2^b..2^b-1} of Sec. 3.1) and a
+ * scale per entry s_ij (per row and/or column, Sec. 3.1; the caller expands
+ * row, group and column scales), i.e.
+ *   c = clamp(rint(x), lo, hi),   x = W~_ij / s_ij,   v = s_ij * c.
  * Ties are broken half-to-even (App. B asks only for a fixed tie rule).
  * The paper's timed runs are float32 (Sec. 6), so the integer decision is
  * taken on x rounded to float32; x itself is reported in fp64.
- * A zero scale means the row's alphabet is {0}.
+ * A zero scale means the entry's alphabet is {0}.
  *
  * Optional tie forcing (the parity protocol): where the oracle's own x lies
- * within tie_window grid steps of a rounding boundary k+1/2 (k in [-l, l-1]),
- * the code given in `forced` is adopted instead and the entry is counted as
- * excused; both choices are valid outputs of the sequential rule up to the
- * tie convention.
+ * within tie_window grid steps of a rounding boundary k+1/2 (k in
+ * [lo, hi-1]), the code given in `forced` is adopted instead and the entry is
+ * counted as excused; both choices are valid outputs of the sequential rule
+ * up to the tie convention.
  */
 #include <math.h>
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
 
-static int quantise_code(double x, int qmax)
+static int quantise_code(double x, int qlo, int qhi)
 {
     float xf = (float)x;
     float r = rintf(xf);             /* half-to-even under the default FE mode */
-    if (r > (float)qmax) r = (float)qmax;
-    if (r < (float)-qmax) r = (float)-qmax;
+    if (r > (float)qhi) r = (float)qhi;
+    if (r < (float)qlo) r = (float)qlo;
     return (int)r;
 }
 
-static int near_boundary(double x, int qmax, double window)
+static int near_boundary(double x, int qlo, int qhi, double window)
 {
     if (!(window > 0.0)) return 0;
-    /* boundaries are k + 1/2 for k = -qmax .. qmax-1 */
+    /* boundaries are k + 1/2 for k = qlo .. qhi-1 */
     double k = floor(x);
     double d = fabs(x - (k + 0.5));
     if (d >= window) return 0;
-    return (k >= -qmax && k <= qmax - 1) ? 1 : 0;
+    return (k >= qlo && k <= qhi - 1) ? 1 : 0;
 }
 
 /*
@@ -59,15 +62,16 @@ static int near_boundary(double x, int qmax, double window)
  *   W0  : m x n row-major input weights
  *   LA  : n x n row-major, unit lower triangular (normalised Cholesky(A^-1))
  *   LB  : m x m row-major, unit lower triangular (normalised Cholesky(B^-1))
- *   scale: m per-row scales (>= 0)
+ *   S   : m x n row-major per-entry scales (>= 0)
+ *   qlo, qhi: the alphabet {qlo..qhi}
  *   forced: NULL, or m x n codes to adopt at near-boundary entries
- * Outputs: codes (m x n), V = s_i * code (m x n), pre = x = W~/s (m x n; NaN
- * for zero-scale rows), counters.  Returns 0, or -1 on allocation failure.
+ * Outputs: codes (m x n), V = s_ij * code (m x n), pre = x = W~/s (m x n; NaN
+ * for zero scales), counters.  Returns 0, or -1 on allocation failure.
  * max_entries > 0 stops after that many entries in visiting order (a bounded
  * timing sample; later outputs are left untouched); <= 0 processes all.
  */
 int oracle_babai_naive(int64_t m, int64_t n, const double *W0, const double *LA,
-                       const double *LB, const double *scale, int qmax,
+                       const double *LB, const double *S, int qlo, int qhi,
                        const int8_t *forced, double tie_window, int8_t *codes,
                        double *V, double *pre, int64_t *n_excused, int64_t *n_flip,
                        int64_t max_entries)
@@ -82,10 +86,10 @@ int oracle_babai_naive(int64_t m, int64_t n, const double *W0, const double *LA,
     int64_t exc = 0, flip = 0, done = 0;
 
     for (int64_t i = 0; i < m; ++i) {
-        const double s = scale[i];
         for (int64_t j = 0; j < n; ++j) {
             if (max_entries > 0 && done >= max_entries) goto out;
             ++done;
+            const double s = S[i * n + j];
             const double w = W[i * n + j];
             int c;
             double x;
@@ -94,8 +98,8 @@ int oracle_babai_naive(int64_t m, int64_t n, const double *W0, const double *LA,
                 x = NAN;
             } else {
                 x = w / s;
-                c = quantise_code(x, qmax);
-                if (forced && near_boundary(x, qmax, tie_window)) {
+                c = quantise_code(x, qlo, qhi);
+                if (forced && near_boundary(x, qlo, qhi, tie_window)) {
                     ++exc;
                     if ((int)forced[i * n + j] != c) ++flip;
                     c = (int)forced[i * n + j];
@@ -136,7 +140,7 @@ out:
  * Tie forcing as for oracle_babai_naive.
  */
 int oracle_ar1_diffusion(int64_t m, int64_t n, const double *W0, double rhoA,
-                         double rhoB, const double *scale, int qmax, const int8_t *forced,
+                         double rhoB, const double *S, int qlo, int qhi, const int8_t *forced,
                          double tie_window, int8_t *codes, double *V, double *pre,
                          int64_t *n_excused, int64_t *n_flip)
 {
@@ -144,8 +148,8 @@ int oracle_ar1_diffusion(int64_t m, int64_t n, const double *W0, double rhoA,
     if (!E) return -1;
     int64_t exc = 0, flip = 0;
     for (int64_t p = 0; p < m; ++p) {
-        const double s = scale[p];
         for (int64_t q = 0; q < n; ++q) {
+            const double s = S[p * n + q];
             double wt = W0[p * n + q];
             if (p > 0) wt -= rhoB * E[(p - 1) * n + q];
             if (q > 0) wt -= rhoA * E[p * n + q - 1];
@@ -155,8 +159,8 @@ int oracle_ar1_diffusion(int64_t m, int64_t n, const double *W0, double rhoA,
             if (s == 0.0) { c = 0; x = NAN; }
             else {
                 x = wt / s;
-                c = quantise_code(x, qmax);
-                if (forced && near_boundary(x, qmax, tie_window)) {
+                c = quantise_code(x, qlo, qhi);
+                if (forced && near_boundary(x, qlo, qhi, tie_window)) {
                     ++exc;
                     if ((int)forced[p * n + q] != c) ++flip;
                     c = (int)forced[p * n + q];

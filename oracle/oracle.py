@@ -21,6 +21,13 @@ Contents, each following a passage of arXiv 2608.06291:
   (Sec. 3.1 definition of RevCholesky), and the pre-rounding values are
   ``W~ = V - E``.  V is a valid sequential-rounding output iff
   ``V = quantise(W~)`` entrywise up to ties.
+* :func:`alphabet_bounds`, :func:`entry_scales` -- the quantiser of Sec. 3.1:
+  an alphabet {lo..hi} (symmetric, or the (b+1)-bit {-2^b..2^b-1}) and
+  scales per row and/or column (row or column-group scales times column
+  factors).
+* :func:`mse_scales` -- App. D's scale choice: max-abs per row over the
+  largest positive code, shrunk by up to 2x where that lowers the row's
+  squared round-to-nearest error.
 * :func:`objective` -- ``tr((W - V)^T B (W - V) A)``, which equals
   ``vec(W - V)^T (A (x) B) vec(W - V)`` by Prop. 3.1.
 """
@@ -60,12 +67,12 @@ def _load():
         i64p = ctypes.POINTER(ctypes.c_int64)
         lib.oracle_babai_naive.restype = ctypes.c_int
         lib.oracle_babai_naive.argtypes = [
-            ctypes.c_int64, ctypes.c_int64, dp, dp, dp, dp, ctypes.c_int,
+            ctypes.c_int64, ctypes.c_int64, dp, dp, dp, dp, ctypes.c_int, ctypes.c_int,
             i8p, ctypes.c_double, i8p, dp, dp, i64p, i64p, ctypes.c_int64]
         lib.oracle_ar1_diffusion.restype = ctypes.c_int
         lib.oracle_ar1_diffusion.argtypes = [
             ctypes.c_int64, ctypes.c_int64, dp, ctypes.c_double, ctypes.c_double,
-            dp, ctypes.c_int, i8p, ctypes.c_double, i8p, dp, dp, i64p, i64p]
+            dp, ctypes.c_int, ctypes.c_int, i8p, ctypes.c_double, i8p, dp, dp, i64p, i64p]
         _lib = lib
     return _lib
 
@@ -81,6 +88,40 @@ def _i8ptr(a):
 def qmax_of_bits(bits: int) -> int:
     """Symmetric alphabet {-l..l} with l = 2^(bits-1) - 1 (App. D uses l = 3)."""
     return (1 << (int(bits) - 1)) - 1
+
+
+def alphabet_bounds(bits: int, alphabet: str = "sym"):
+    """(lo, hi) of the quantisation alphabet {lo..hi} (Sec. 3.1): "sym" is
+    {-l..l}, l = 2^(bits-1) - 1 (App. D); "asym" is the (b+1)-bit alphabet
+    {-2^b .. 2^b - 1} with b = bits - 1."""
+    if alphabet == "sym":
+        l = qmax_of_bits(bits)
+        return -l, l
+    if alphabet == "asym":
+        h = 1 << (int(bits) - 1)
+        return -h, h - 1
+    raise ValueError(alphabet)
+
+
+def entry_scales(scale, m: int, n: int, group_size: int = 0, col_scale=None) -> np.ndarray:
+    """Per-entry scales s_ij (Sec. 3.1: factors per row and/or column).
+
+    scale: m per-row scales, or with group_size g > 0 an m x ceil(n/g) matrix
+    of per-(row, column group) scales (group of column j: j // g); an m x n
+    array is taken as given.  col_scale: None or n per-column factors, which
+    multiply the row/group scale in fp32 (the stored scales are fp32).
+    Returned as fp64 holding the fp32 values."""
+    S = np.asarray(scale, dtype=np.float32)
+    if S.shape == (m, n) and group_size == 0 and col_scale is None:
+        return S.astype(np.float64)
+    if group_size > 0:
+        G = -(-n // group_size)
+        base = S.reshape(m, G)[:, np.arange(n) // group_size]
+    else:
+        base = np.broadcast_to(S.reshape(m, 1), (m, n))
+    if col_scale is not None:
+        base = (base * np.asarray(col_scale, dtype=np.float32).reshape(1, n)).astype(np.float32)
+    return np.ascontiguousarray(base, dtype=np.float64)
 
 
 def damp(X, lam: float) -> np.ndarray:
@@ -110,16 +151,18 @@ def rev_cholesky(Xd) -> np.ndarray:
 
 
 def babai(W, LA, LB, scale, bits: int, forced=None, tie_window: float = 0.0,
-          max_entries: int = 0):
+          max_entries: int = 0, alphabet: str = "sym"):
     """Sequential rounding of Alg. 2 (row-major), in C.  Returns a dict with
     codes (int8), V (fp64), pre (x = W~/s, fp64), n_excused, n_flip.
+    scale: per-row (m) or per-entry (m x n, see :func:`entry_scales`).
     max_entries > 0 stops after that many entries (timing samples only)."""
     lib = _load()
     W = np.ascontiguousarray(W, dtype=np.float64)
     m, n = W.shape
     LA = np.ascontiguousarray(LA, dtype=np.float64)
     LB = np.ascontiguousarray(LB, dtype=np.float64)
-    s = np.ascontiguousarray(scale, dtype=np.float64).reshape(m)
+    s = entry_scales(scale, m, n)
+    qlo, qhi = alphabet_bounds(bits, alphabet)
     assert LA.shape == (n, n) and LB.shape == (m, m)
     codes = np.zeros((m, n), np.int8)
     V = np.zeros((m, n), np.float64)
@@ -132,7 +175,7 @@ def babai(W, LA, LB, scale, bits: int, forced=None, tie_window: float = 0.0,
         assert forced.shape == (m, n)
         fp = _i8ptr(forced)
     rc = lib.oracle_babai_naive(m, n, _dptr(W), _dptr(LA), _dptr(LB), _dptr(s),
-                                qmax_of_bits(bits), fp, float(tie_window),
+                                qlo, qhi, fp, float(tie_window),
                                 _i8ptr(codes), _dptr(V), _dptr(pre),
                                 ctypes.byref(exc), ctypes.byref(flip), int(max_entries))
     if rc != 0:
@@ -142,13 +185,14 @@ def babai(W, LA, LB, scale, bits: int, forced=None, tie_window: float = 0.0,
 
 
 def solve(W, A, B, damp_lambda: float, scale, bits: int, forced=None,
-          tie_window: float = 0.0):
+          tie_window: float = 0.0, alphabet: str = "sym"):
     """Factors by the literal route, then :func:`babai`.  B=None means I_m."""
     W = np.asarray(W, dtype=np.float64)
     m, n = W.shape
     LA = normalized_factor(A, damp_lambda)
     LB = np.eye(m) if B is None else normalized_factor(B, damp_lambda)
-    return babai(W, LA, LB, scale, bits, forced=forced, tie_window=tie_window)
+    return babai(W, LA, LB, scale, bits, forced=forced, tie_window=tie_window,
+                 alphabet=alphabet)
 
 
 def naive_macs(m: int, n: int, entries: int | None = None) -> float:
@@ -165,12 +209,13 @@ def naive_macs(m: int, n: int, entries: int | None = None) -> float:
 
 
 def ar1_diffusion(W, rhoA: float, rhoB: float, scale, bits: int, forced=None,
-                  tie_window: float = 0.0):
+                  tie_window: float = 0.0, alphabet: str = "sym"):
     """Exact output for A = [rhoA^|i-j|], B = [rhoB^|i-j|] without damping."""
     lib = _load()
     W = np.ascontiguousarray(W, dtype=np.float64)
     m, n = W.shape
-    s = np.ascontiguousarray(scale, dtype=np.float64).reshape(m)
+    s = entry_scales(scale, m, n)
+    qlo, qhi = alphabet_bounds(bits, alphabet)
     codes = np.zeros((m, n), np.int8)
     V = np.zeros((m, n), np.float64)
     pre = np.zeros((m, n), np.float64)
@@ -182,30 +227,30 @@ def ar1_diffusion(W, rhoA: float, rhoB: float, scale, bits: int, forced=None,
         assert forced.shape == (m, n)
         fp = _i8ptr(forced)
     rc = lib.oracle_ar1_diffusion(m, n, _dptr(W), float(rhoA), float(rhoB), _dptr(s),
-                                  qmax_of_bits(bits), fp, float(tie_window), _i8ptr(codes),
+                                  qlo, qhi, fp, float(tie_window), _i8ptr(codes),
                                   _dptr(V), _dptr(pre), ctypes.byref(exc), ctypes.byref(flip))
     if rc != 0:
         raise MemoryError("oracle_ar1_diffusion: allocation failed")
     return dict(codes=codes, V=V, pre=pre, n_excused=int(exc.value), n_flip=int(flip.value))
 
 
-def near_boundary(x, bits: int, window: float) -> np.ndarray:
+def near_boundary(x, bits: int, window: float, alphabet: str = "sym") -> np.ndarray:
     """Entries whose grid value x lies within `window` of a boundary k+1/2,
-    k in [-l, l-1]; NaN (zero-scale rows) is never near a boundary."""
-    l = qmax_of_bits(bits)
+    k in [lo, hi-1]; NaN (zero scale) is never near a boundary."""
+    lo, hi = alphabet_bounds(bits, alphabet)
     x = np.asarray(x, dtype=np.float64)
     k = np.floor(x)
     with np.errstate(invalid="ignore"):
-        near = (np.abs(x - (k + 0.5)) < window) & (k >= -l) & (k <= l - 1)
+        near = (np.abs(x - (k + 0.5)) < window) & (k >= lo) & (k <= hi - 1)
     return near & np.isfinite(x)
 
 
-def quantise_codes(x, bits: int) -> np.ndarray:
-    """clamp(rint(float32(x)), -l, l); NaN (zero scale) maps to 0."""
-    l = qmax_of_bits(bits)
+def quantise_codes(x, bits: int, alphabet: str = "sym") -> np.ndarray:
+    """clamp(rint(float32(x)), lo, hi); NaN (zero scale) maps to 0."""
+    lo, hi = alphabet_bounds(bits, alphabet)
     xf = np.asarray(x, dtype=np.float64).astype(np.float32)
     with np.errstate(invalid="ignore"):
-        c = np.clip(np.rint(xf), -l, l)
+        c = np.clip(np.rint(xf), lo, hi)
     c = np.where(np.isfinite(xf), c, 0)
     return c.astype(np.int8)
 
@@ -220,8 +265,8 @@ def certificate(W, A, B, damp_lambda: float, scale, codes, bits: int,
     """
     W = np.asarray(W, dtype=np.float64)
     m, n = W.shape
-    s = np.asarray(scale, dtype=np.float64).reshape(m)
-    V = s[:, None] * np.asarray(codes, dtype=np.float64)
+    S = entry_scales(scale, m, n)
+    V = S * np.asarray(codes, dtype=np.float64)
     if RA is None:
         RA = rev_cholesky(damp(A, damp_lambda))
     if B is None:
@@ -239,20 +284,20 @@ def certificate(W, A, B, damp_lambda: float, scale, codes, bits: int,
         E = (RhB[rows, :] @ D) @ RhA.T
         Vr = V[rows]
     Wt = Vr - E
-    sr = s if rows is None else s[rows]
+    Sr = S if rows is None else S[rows]
     with np.errstate(divide="ignore", invalid="ignore"):
-        x = Wt / sr[:, None]
-    x[sr == 0.0, :] = np.nan
+        x = Wt / Sr
+    x[Sr == 0.0] = np.nan
     return x
 
 
-def verdict(codes, x, bits: int, window: float = 1e-4):
+def verdict(codes, x, bits: int, window: float = 1e-4, alphabet: str = "sym"):
     """Compare candidate codes with quantise(x) along the candidate's own
     trajectory.  violations: differ and not near a boundary (must be 0);
     flips: differ at near-boundary entries (excused, rate-limited)."""
     codes = np.asarray(codes)
-    own = quantise_codes(x, bits)
-    near = near_boundary(x, bits, window)
+    own = quantise_codes(x, bits, alphabet)
+    near = near_boundary(x, bits, window, alphabet)
     diff = own != codes
     return dict(violations=int(np.count_nonzero(diff & ~near)),
                 flips=int(np.count_nonzero(diff & near)),
@@ -266,3 +311,38 @@ def objective(W, V, A, B, damp_lambda: float) -> float:
     Ad = damp(A, damp_lambda)
     BD = D if B is None else damp(B, damp_lambda) @ D
     return float(np.sum(BD * (D @ Ad)))
+
+
+def mse_scale_candidates(W, bits: int, alphabet: str = "sym", grid: int = 100,
+                         maxshrink: float = 0.5) -> np.ndarray:
+    """Candidate scales of every row, m x (grid + 1), fp32 values (App. D):
+    s_k = fl32(fl32(max_j |W_ij| / hi) * p_k), p_k = fl32(1 - maxshrink k / grid),
+    hi the largest positive code of the alphabet."""
+    W32 = np.asarray(W, dtype=np.float32)
+    _, hi = alphabet_bounds(bits, alphabet)
+    base = (np.max(np.abs(W32), axis=1) / np.float32(hi)).astype(np.float32)
+    p = np.array([1.0 - maxshrink * k / grid for k in range(grid + 1)]).astype(np.float32)
+    return (base[:, None] * p[None, :]).astype(np.float32)
+
+
+def mse_scales(W, bits: int, alphabet: str = "sym", grid: int = 100,
+               maxshrink: float = 0.5):
+    """App. D: per row, the candidate scale (max-abs over the largest code,
+    shrunk by p_k in [1 - maxshrink, 1]) whose round-to-nearest quantisation
+    has the least squared error sum_j (W_ij - fl32(s c_ij))^2, with
+    c_ij = clamp(rint(fl32(W_ij / s)), lo, hi); the first (least shrunk)
+    candidate wins ties.  Returns (scales fp32 (m), errors fp64 (m, grid+1))."""
+    W32 = np.asarray(W, dtype=np.float32)
+    m, n = W32.shape
+    lo, hi = alphabet_bounds(bits, alphabet)
+    cand = mse_scale_candidates(W32, bits, alphabet, grid, maxshrink)
+    err = np.zeros((m, grid + 1), np.float64)
+    for k in range(grid + 1):
+        s = cand[:, k:k + 1]
+        with np.errstate(divide="ignore", invalid="ignore"):
+            x = (W32 / s).astype(np.float32)
+        c = np.where(s > 0, np.clip(np.rint(x), lo, hi), 0).astype(np.float32)
+        v = (s * c).astype(np.float32)
+        err[:, k] = np.sum((W32.astype(np.float64) - v.astype(np.float64)) ** 2, axis=1)
+    best = np.argmin(err, axis=1)       # first minimum
+    return cand[np.arange(m), best].astype(np.float32), err
