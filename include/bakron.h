@@ -11,8 +11,8 @@
  * current value, and feeding the error back to the later entries through
  * the unit-lower factors L^A = normalised Cholesky(A^-1) and
  * L^B = normalised Cholesky(B^-1).  "round" is replaced by quantisation to
- * the symmetric alphabet {-l..l}, l = 2^(bits-1) - 1, with a per-row scale
- * (Sec. 3.1; App. D), ties to even.
+ * an integer alphabet with scales per row, column or column group
+ * (Sec. 3.1; App. D; see bakron_quantizer), ties to even.
  *
  * Conventions for every entry point:
  *   - All matrices are row-major, contiguous, fp32 unless stated otherwise.
@@ -47,13 +47,38 @@ typedef enum {
  * fp32 plus the cached solve workspace for the last (m, n) solved. */
 typedef struct bakron_factors bakron_factors;
 
-/* Quantiser (Sec. 3.1; App. D): alphabet {-l..l} with l = 2^(bits-1) - 1,
- * bits in [2, 8]; scale is a DEVICE pointer to m fp32 per-row scales
- * s_i >= 0 (s_i = 0 means the row's alphabet is {0}).  The caller chooses
- * the scales (App. D uses max_j |W_ij| / l). */
+/* Quantisation alphabets (Sec. 3.1).  bits in [2, 8]; h = 2^(bits-1):
+ *   SYMMETRIC   {-(h-1) .. h-1}  (App. D's {-l..l}, l = h - 1)
+ *   ASYMMETRIC  {-h .. h-1}      (the (b+1)-bit alphabet {-2^b .. 2^b-1}) */
+typedef enum {
+    BAKRON_ALPHABET_SYMMETRIC = 0,
+    BAKRON_ALPHABET_ASYMMETRIC = 1
+} bakron_alphabet;
+
+/* Quantiser (Sec. 3.1: scaling factors per row and/or column; App. D).
+ * Entry (i, j) is quantised as c = clamp(rint(W~_ij / s_ij), lo, hi) and
+ * V_ij = s_ij * c, with the scale
+ *   s_ij = base_ij * (col_scale ? col_scale[j] : 1)     (one fp32 product)
+ *   base_ij = group_size > 0 ? scale[i * ceil(n / group_size) + j / group_size]
+ *                            : scale[i]
+ * All scales are >= 0; s_ij = 0 makes the entry's alphabet {0}.  The caller
+ * chooses the scales (App. D: max_j |W_ij| / l per row, optionally shrunk by
+ * an MSE search: bakron_mse_scales).
+ *   bits        alphabet size, in [2, 8]
+ *   scale       DEVICE pointer: m per-row scales (group_size = 0), or an
+ *               m x ceil(n / group_size) row-major matrix of per-(row, column
+ *               group) scales
+ *   alphabet    bakron_alphabet
+ *   group_size  0, or the number of consecutive columns sharing a scale
+ *   col_scale   DEVICE pointer to n per-column factors, or NULL
+ * Zero-initialise the struct and set bits and scale for the per-row symmetric
+ * quantiser of App. D. */
 typedef struct {
     int32_t bits;
     const float *scale;
+    int32_t alphabet;
+    int32_t group_size;
+    const float *col_scale;
 } bakron_quantizer;
 
 /*
@@ -85,9 +110,9 @@ bakron_status bakron_factor(const float *A, int64_t n, const float *B, int64_t m
  *   W      device, m x n, not modified
  *   m, n   must equal the handle's sizes (n always; m when B was given)
  *   f      handle from bakron_factor
- *   q      quantiser; q.scale is a device pointer to m floats
- *   codes  device, m x n int8 output in [-l, l]
- *   V      device, m x n fp32 output, V_ij = s_i * codes_ij (one fp32 product)
+ *   q      quantiser (alphabet and scales, see bakron_quantizer)
+ *   codes  device, m x n int8 output in the alphabet
+ *   V      device, m x n fp32 output, V_ij = s_ij * codes_ij (one fp32 product)
  *
  * The first call for a given (m, n) allocates the workspace (about 8*m*n
  * bytes plus one int per 32 x 32 tile) and builds the launch plans; later
@@ -108,8 +133,8 @@ bakron_status bakron_solve(const float *W, int64_t m, int64_t n, const bakron_fa
 
 /*
  * bakron_solve_debug -- bakron_solve that also writes, for every entry, the
- * pre-rounding value in grid units x_ij = W~_ij / s_i (device, m x n fp32;
- * NaN on zero-scale rows), the value at which the entry was quantised.
+ * pre-rounding value in grid units x_ij = W~_ij / s_ij (device, m x n fp32;
+ * NaN where s_ij = 0), the value at which the entry was quantised.
  * Used to measure the numerical margin against the fp64 oracle.
  */
 bakron_status bakron_solve_debug(const float *W, int64_t m, int64_t n, const bakron_factors *f,
@@ -135,6 +160,45 @@ bakron_status bakron_solve_debug(const float *W, int64_t m, int64_t n, const bak
 bakron_status bakron_solve_antidiag(const float *W, int64_t m, int64_t n, const bakron_factors *f,
                                     bakron_quantizer q, int8_t *codes, float *V, float *pre,
                                     hipStream_t stream);
+
+/*
+ * bakron_factor_blockdiag -- bakron_factor with an output factor that is
+ * block-diagonal, B = blockdiag(B_0, .., B_{nblocks-1}): the per-head output
+ * Grams of an attention projection assembled into one matrix spanning the
+ * whole projection (App. D; BaKron puts no block structure on B, and
+ * errors then never propagate between heads).
+ *   B_blocks  device, nblocks x hb x hb (block h row-major at h * hb * hb),
+ *             each symmetric PSD; m = nblocks * hb, at most 2^20
+ *   damp      relative to the mean diagonal of the assembled B (all blocks),
+ *             as in bakron_factor
+ * Other arguments, results and errors as bakron_factor.  Assembles B in a
+ * temporary m x m fp32 device buffer (freed before returning).
+ */
+bakron_status bakron_factor_blockdiag(const float *A, int64_t n, const float *B_blocks,
+                                      int64_t nblocks, int64_t hb, float damp, hipStream_t stream,
+                                      bakron_factors **out);
+
+/*
+ * bakron_mse_scales -- App. D's scale choice: for each row (group_size = 0)
+ * or each (row, group of group_size columns) of W, the scale
+ *   s_k = fl32(base * p_k),  base = fl32(max |W_ij| / hi),
+ *   p_k = fl32(1 - maxshrink * k / grid),  k = 0 .. grid
+ * (hi the alphabet's largest code) that minimises the squared error of
+ * round-to-nearest quantisation, sum_j (W_ij - fl32(s_k c_ij))^2 with
+ * c_ij = clamp(rint(fl32(W_ij / s_k)), lo, hi), summed in fp64; the first
+ * minimum (least shrink) wins.  grid = 0 gives the max-abs scale.
+ *   W          device, m x n fp32
+ *   bits, alphabet  as bakron_quantizer
+ *   group_size 0 or the column-group width
+ *   grid       in [0, 255] (App. D's "shrink by up to 2x": maxshrink 0.5)
+ *   maxshrink  in [0, 1)
+ *   scale      device output: m floats, or m x ceil(n / group_size), usable
+ *              as bakron_quantizer.scale
+ * One launch on `stream`.  Errors: BAKRON_EINVAL for bad arguments.
+ */
+bakron_status bakron_mse_scales(const float *W, int64_t m, int64_t n, int32_t bits,
+                                int32_t alphabet, int32_t group_size, int32_t grid,
+                                double maxshrink, float *scale, hipStream_t stream);
 
 /* Frees the handle, its factors and its workspace (synchronises the device
  * work that used them).  NULL is a no-op. */

@@ -317,27 +317,36 @@ def mse_scale_candidates(W, bits: int, alphabet: str = "sym", grid: int = 100,
                          maxshrink: float = 0.5) -> np.ndarray:
     """Candidate scales of every row, m x (grid + 1), fp32 values (App. D):
     s_k = fl32(fl32(max_j |W_ij| / hi) * p_k), p_k = fl32(1 - maxshrink k / grid),
-    hi the largest positive code of the alphabet."""
+    hi the largest positive code of the alphabet (grid = 0: s = the base)."""
     W32 = np.asarray(W, dtype=np.float32)
     _, hi = alphabet_bounds(bits, alphabet)
     base = (np.max(np.abs(W32), axis=1) / np.float32(hi)).astype(np.float32)
+    if grid == 0:
+        return base[:, None].copy()
     p = np.array([1.0 - maxshrink * k / grid for k in range(grid + 1)]).astype(np.float32)
     return (base[:, None] * p[None, :]).astype(np.float32)
 
 
 def mse_scales(W, bits: int, alphabet: str = "sym", grid: int = 100,
-               maxshrink: float = 0.5):
+               maxshrink: float = 0.5, group_size: int = 0):
     """App. D: per row, the candidate scale (max-abs over the largest code,
     shrunk by p_k in [1 - maxshrink, 1]) whose round-to-nearest quantisation
     has the least squared error sum_j (W_ij - fl32(s c_ij))^2, with
     c_ij = clamp(rint(fl32(W_ij / s)), lo, hi); the first (least shrunk)
-    candidate wins ties.  Returns (scales fp32 (m), errors fp64 (m, grid+1))."""
+    candidate wins ties.  With group_size g > 0 the same per (row, group of g
+    columns), giving m x ceil(n/g) scales.  Returns (scales fp32, errors fp64
+    (rows x segments x (grid + 1)) or (m, grid + 1) without groups)."""
     W32 = np.asarray(W, dtype=np.float32)
     m, n = W32.shape
+    if group_size > 0:
+        outs = [mse_scales(W32[:, g0:g0 + group_size], bits, alphabet, grid, maxshrink)
+                for g0 in range(0, n, group_size)]
+        return (np.stack([o[0] for o in outs], axis=1),
+                np.stack([o[1] for o in outs], axis=1))
     lo, hi = alphabet_bounds(bits, alphabet)
     cand = mse_scale_candidates(W32, bits, alphabet, grid, maxshrink)
-    err = np.zeros((m, grid + 1), np.float64)
-    for k in range(grid + 1):
+    err = np.zeros((m, cand.shape[1]), np.float64)
+    for k in range(cand.shape[1]):
         s = cand[:, k:k + 1]
         with np.errstate(divide="ignore", invalid="ignore"):
             x = (W32 / s).astype(np.float32)

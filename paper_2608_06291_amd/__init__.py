@@ -5,6 +5,7 @@ The solver itself is hand-written HIP for gfx950 behind a C ABI
 """
 from ._lib import (BAKRON_EHIP, BAKRON_EINVAL, BAKRON_ENOMEM, BAKRON_ENOTSPD, BAKRON_OK,  # noqa: F401
                    BAKRON_KFAC, BAKRON_SHAMPOO,
-                   EXPORTED, LIB_PATH, BakronError, Factors, factor, gram, gram_workspace_bytes,
+                   EXPORTED, LIB_PATH, BakronError, Factors, factor, factor_blockdiag, gram,
+                   gram_workspace_bytes, mse_scales,
                    kron_factors, load, mlp_local_factors, sample_weights, solve, solve_antidiag,
                    status_string)

@@ -18,7 +18,10 @@ EXPORTED = ("bakron_factor", "bakron_solve", "bakron_solve_debug", "bakron_facto
             "bakron_status_string", "bakron_factors_error", "bakron_last_error",
             "bakron_factor_export", "bakron_profile_enable", "bakron_profile_read",
             "bakron_solve_check", "bakron_solve_antidiag", "bakron_gram",
-            "bakron_sample_weights", "bakron_kron_factors", "bakron_mlp_local_factors")
+            "bakron_sample_weights", "bakron_kron_factors", "bakron_mlp_local_factors",
+            "bakron_mse_scales", "bakron_factor_blockdiag")
+
+ALPHABETS = {"sym": 0, "asym": 1}
 
 BAKRON_KFAC, BAKRON_SHAMPOO = 0, 1
 STYLES = {"kfac": BAKRON_KFAC, "shampoo": BAKRON_SHAMPOO}
@@ -33,7 +36,8 @@ class BakronError(RuntimeError):
 
 
 class _Quantizer(ctypes.Structure):
-    _fields_ = [("bits", ctypes.c_int32), ("scale", ctypes.c_void_p)]
+    _fields_ = [("bits", ctypes.c_int32), ("scale", ctypes.c_void_p), ("alphabet", ctypes.c_int32),
+                ("group_size", ctypes.c_int32), ("col_scale", ctypes.c_void_p)]
 
 
 class KernelStat(ctypes.Structure):
@@ -82,6 +86,12 @@ def load(path: str = LIB_PATH):
     lib.bakron_solve_check.restype = ctypes.c_int
     lib.bakron_solve_check.argtypes = [vp, vp, ctypes.POINTER(ctypes.c_int32)]
     i64, szp = ctypes.c_int64, ctypes.POINTER(ctypes.c_size_t)
+    lib.bakron_mse_scales.restype = ctypes.c_int
+    lib.bakron_mse_scales.argtypes = [vp, i64, i64, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+                                      ctypes.c_int32, ctypes.c_double, vp, vp]
+    lib.bakron_factor_blockdiag.restype = ctypes.c_int
+    lib.bakron_factor_blockdiag.argtypes = [vp, i64, vp, i64, i64, ctypes.c_float, vp,
+                                            ctypes.POINTER(vp)]
     lib.bakron_gram.restype = ctypes.c_int
     lib.bakron_gram.argtypes = [vp, i64, i64, vp, ctypes.c_float, vp, vp, vp, szp, vp]
     lib.bakron_sample_weights.restype = ctypes.c_int
@@ -203,25 +213,48 @@ def factor(A, B, damp: float) -> Factors:
     return Factors(h.value, n, m if B is not None else None, A.device)
 
 
-def solve(W, f: Factors, bits: int, scale, codes=None, V=None, pre=None, debug: bool = False):
+def _quantizer(bits, scale, m, n, alphabet, group_size, col_scale):
+    """bakron_quantizer for per-row (m) or per-(row, group) (m x ceil(n/g))
+    scales, optional per-column factors, alphabet "sym" or "asym"."""
+    import torch
+    _check_dev(scale, "scale", torch.float32)
+    g = int(group_size)
+    if g < 0:
+        raise ValueError("group_size must be >= 0")
+    want = m * (-(-n // g)) if g > 0 else m
+    if scale.numel() != want:
+        raise ValueError(f"scale must have {want} entries")
+    cp = None
+    if col_scale is not None:
+        _check_dev(col_scale, "col_scale", torch.float32)
+        if col_scale.numel() != n:
+            raise ValueError("col_scale must have n entries")
+        cp = col_scale.data_ptr()
+    if alphabet not in ALPHABETS:
+        raise ValueError(f"alphabet must be one of {sorted(ALPHABETS)}")
+    return _Quantizer(int(bits), ctypes.c_void_p(scale.data_ptr()).value, ALPHABETS[alphabet], g,
+                      cp)
+
+
+def solve(W, f: Factors, bits: int, scale, codes=None, V=None, pre=None, debug: bool = False,
+          alphabet: str = "sym", group_size: int = 0, col_scale=None):
     """bakron_solve / bakron_solve_debug on the current stream.
 
+    scale: m per-row scales, or m x ceil(n / group_size) with group_size > 0;
+    col_scale: None or n per-column factors; alphabet "sym" or "asym".
     Returns (codes int8, V fp32) or (codes, V, pre) when debug=True.
     """
     import torch
     lib = load()
     _check_dev(W, "W", torch.float32)
-    _check_dev(scale, "scale", torch.float32)
     m, n = W.shape
-    if scale.numel() != m:
-        raise ValueError("scale must have m entries")
+    q = _quantizer(bits, scale, m, n, alphabet, group_size, col_scale)
     if codes is None:
         codes = torch.empty((m, n), dtype=torch.int8, device=W.device)
     if V is None:
         V = torch.empty((m, n), dtype=torch.float32, device=W.device)
     _check_dev(codes, "codes", torch.int8)
     _check_dev(V, "V", torch.float32)
-    q = _Quantizer(int(bits), ctypes.c_void_p(scale.data_ptr()).value)
     s = _stream(torch, W.device)
     if debug:
         if pre is None:
@@ -238,18 +271,18 @@ def solve(W, f: Factors, bits: int, scale, codes=None, V=None, pre=None, debug: 
     return (codes, V, pre) if debug else (codes, V)
 
 
-def solve_antidiag(W, f: Factors, bits: int, scale, codes=None, V=None, pre=None):
+def solve_antidiag(W, f: Factors, bits: int, scale, codes=None, V=None, pre=None,
+                   alphabet: str = "sym", group_size: int = 0, col_scale=None):
     """bakron_solve_antidiag (BaKron-antidiagonal, Alg. 3) on the current stream.
 
+    Quantiser arguments as :func:`solve`.
     Returns (codes int8, V fp32), or (codes, V, pre) when a pre buffer is given.
     """
     import torch
     lib = load()
     _check_dev(W, "W", torch.float32)
-    _check_dev(scale, "scale", torch.float32)
     m, n = W.shape
-    if scale.numel() != m:
-        raise ValueError("scale must have m entries")
+    q = _quantizer(bits, scale, m, n, alphabet, group_size, col_scale)
     if codes is None:
         codes = torch.empty((m, n), dtype=torch.int8, device=W.device)
     if V is None:
@@ -258,7 +291,6 @@ def solve_antidiag(W, f: Factors, bits: int, scale, codes=None, V=None, pre=None
     _check_dev(V, "V", torch.float32)
     if pre is not None:
         _check_dev(pre, "pre", torch.float32)
-    q = _Quantizer(int(bits), ctypes.c_void_p(scale.data_ptr()).value)
     st = lib.bakron_solve_antidiag(ctypes.c_void_p(W.data_ptr()), m, n, f.handle, q,
                                    ctypes.c_void_p(codes.data_ptr()), ctypes.c_void_p(V.data_ptr()),
                                    ctypes.c_void_p(pre.data_ptr() if pre is not None else None),
@@ -266,6 +298,42 @@ def solve_antidiag(W, f: Factors, bits: int, scale, codes=None, V=None, pre=None
     if st != BAKRON_OK:
         raise BakronError(st, f.error())
     return (codes, V) if pre is None else (codes, V, pre)
+
+
+def factor_blockdiag(A, B_blocks, damp: float) -> Factors:
+    """bakron_factor_blockdiag: B = blockdiag of B_blocks (nblocks x hb x hb)."""
+    import torch
+    lib = load()
+    _check_dev(A, "A", torch.float32)
+    _check_dev(B_blocks, "B_blocks", torch.float32)
+    n = A.shape[0]
+    if A.shape != (n, n) or B_blocks.dim() != 3 or B_blocks.shape[1] != B_blocks.shape[2]:
+        raise ValueError("A must be n x n and B_blocks nblocks x hb x hb")
+    nb, hb = B_blocks.shape[0], B_blocks.shape[1]
+    h = ctypes.c_void_p(0)
+    st = lib.bakron_factor_blockdiag(ctypes.c_void_p(A.data_ptr()), n,
+                                     ctypes.c_void_p(B_blocks.data_ptr()), nb, hb, float(damp),
+                                     _stream(torch, A.device), ctypes.byref(h))
+    if st != BAKRON_OK:
+        raise BakronError(st, lib.bakron_last_error().decode())
+    return Factors(h.value, n, nb * hb, A.device)
+
+
+def mse_scales(W, bits: int, alphabet: str = "sym", group_size: int = 0, grid: int = 100,
+               maxshrink: float = 0.5):
+    """bakron_mse_scales on the current stream: m scales, or m x ceil(n/g)."""
+    import torch
+    lib = load()
+    _check_dev(W, "W", torch.float32)
+    m, n = W.shape
+    g = int(group_size)
+    out = torch.empty((m, -(-n // g)) if g > 0 else (m,), dtype=torch.float32, device=W.device)
+    st = lib.bakron_mse_scales(ctypes.c_void_p(W.data_ptr()), m, n, int(bits),
+                               ALPHABETS[alphabet], g, int(grid), float(maxshrink),
+                               ctypes.c_void_p(out.data_ptr()), _stream(torch, W.device))
+    if st != BAKRON_OK:
+        raise BakronError(st, lib.bakron_last_error().decode())
+    return out
 
 
 # ---------------------------------------------------------------- factor construction

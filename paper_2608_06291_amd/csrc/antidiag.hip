@@ -5,8 +5,8 @@
 // form of YAQA) and reaches the same output as the BaKron solver (Thm 3.2).
 //
 // For every element anti-diagonal k = 0 .. m+n-2 in order:
-//   round:  for the entries (i, k-i): x = W~/s_i, c = clamp(rint x, -l, l),
-//           V = s_i c, E = V - W~ (the error Delta of Alg. 3);
+//   round:  for the entries (i, k-i): x = W~/s_ij, c = clamp(rint x, lo, hi),
+//           V = s_ij c, E = V - W~ (the error Delta of Alg. 3);
 //   update: W~ += L^B * antidiag_k(E) * L^A^T, i.e. for every (p, q)
 //           W~_pq += sum_i L^B[p][i] E[i][k-i] L^A[q][k-i]  (a rank-r product,
 //           r = number of entries on the diagonal).
@@ -18,19 +18,19 @@ namespace bk {
 
 // Round the entries (i, k - i), i in [i0, i1], of the working copy Wt
 // (row-major m x n); the error of row i goes to delta[i].
-__global__ __launch_bounds__(256) void k_ad_round(const float* __restrict__ Wt, int64_t n, int k,
-                                                  int i0, int i1, const float* __restrict__ scale,
-                                                  float qmax, int8_t* __restrict__ codes,
+__global__ __launch_bounds__(256) void k_ad_round(const float* __restrict__ Wt, int64_t m, int64_t n,
+                                                  int k, int i0, int i1, QuantArgs q,
+                                                  int8_t* __restrict__ codes,
                                                   float* __restrict__ V, float* __restrict__ pre,
                                                   float* __restrict__ delta) {
     const int i = i0 + (int)(blockIdx.x * 256 + threadIdx.x);
     if (i > i1) return;
     const int64_t o = (int64_t)i * n + (k - i);
     const float w = Wt[o];
-    const float s = scale[i];
+    const float s = entry_scale(q, i, k - i, m, n);
     const float inv_s = s > 0.0f ? 1.0f / s : 0.0f;   // zero scale: alphabet {0}
     const float x = w * inv_s;
-    const float c = __builtin_amdgcn_fmed3f(rintf(x), -qmax, qmax);
+    const float c = __builtin_amdgcn_fmed3f(rintf(x), q.qlo, q.qhi);
     codes[o] = (int8_t)(int)c;
     V[o] = c * s;
     if (pre) pre[o] = s > 0.0f ? x : __builtin_nanf("");
@@ -146,8 +146,8 @@ __global__ __launch_bounds__(256) void k_ad_update(float* __restrict__ Wt, int64
 // then round and update one anti-diagonal after the other.  delta holds
 // 32 * ceil(m / 32) floats (one per row, read in whole tile-aligned chunks).
 hipError_t run_antidiag(hipStream_t st, const float* W, int64_t m, int64_t n, float* Wt,
-                        float* delta, const float* LA, const float* LB, const float* scale,
-                        float qmax, int8_t* codes, float* V, float* pre) {
+                        float* delta, const float* LA, const float* LB, const QuantArgs& q,
+                        int8_t* codes, float* V, float* pre) {
     hipError_t e = hipMemcpyAsync(Wt, W, sizeof(float) * (size_t)(m * n), hipMemcpyDeviceToDevice, st);
     if (e != hipSuccess) return e;
     const int nbp = (int)((m + AD_B - 1) / AD_B), nbq = (int)((n + AD_B - 1) / AD_B);
@@ -155,8 +155,8 @@ hipError_t run_antidiag(hipStream_t st, const float* W, int64_t m, int64_t n, fl
         const int i0 = k - (int)(n - 1) > 0 ? k - (int)(n - 1) : 0;
         const int i1 = k < (int)(m - 1) ? k : (int)(m - 1);
         const int cnt = i1 - i0 + 1;
-        hipLaunchKernelGGL(k_ad_round, dim3((unsigned)((cnt + 255) / 256)), dim3(256), 0, st, Wt, n,
-                           k, i0, i1, scale, qmax, codes, V, pre, delta);
+        hipLaunchKernelGGL(k_ad_round, dim3((unsigned)((cnt + 255) / 256)), dim3(256), 0, st, Wt, m,
+                           n, k, i0, i1, q, codes, V, pre, delta);
         if (k < (int)(m + n - 2))
             hipLaunchKernelGGL(k_ad_update, dim3((unsigned)(nbp * nbq)), dim3(256), 0, st, Wt, m, n, k,
                                i0, i1, LA, LB, delta, nbq);

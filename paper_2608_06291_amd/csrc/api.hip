@@ -21,13 +21,13 @@ hipError_t unpack_factor(hipStream_t s, const float* packed, int64_t d, float* d
 
 hipError_t run_plan(hipStream_t st, hipStream_t side, const Plan& plan, const float* W, int64_t m,
                     int64_t n, int mt, int nt, const Workspace& ws, const float* LA, const float* LB,
-                    int b_ident, const float* scale, float qmax, int8_t* codes, float* V, float* pre,
+                    int b_ident, const QuantArgs& q, int8_t* codes, float* V, float* pre,
                     int knear, const int4* items, hipEvent_t* tim, hipEvent_t* ev_rel,
                     hipEvent_t* ev_side);
 int plan_timed_launches(const Plan& plan);
 hipError_t run_antidiag(hipStream_t st, const float* W, int64_t m, int64_t n, float* Wt,
-                        float* delta, const float* LA, const float* LB, const float* scale,
-                        float qmax, int8_t* codes, float* V, float* pre);
+                        float* delta, const float* LA, const float* LB, const QuantArgs& q,
+                        int8_t* codes, float* V, float* pre);
 }  // namespace bk
 
 struct bakron_factors {
@@ -539,6 +539,19 @@ static bakron_status ensure_workspace(bakron_factors* f, int64_t m, int64_t n) {
     return BAKRON_OK;
 }
 
+// the kernels' view of a quantiser (alphabet bounds, scale lookup)
+static bk::QuantArgs quant_args(const bakron_quantizer& q, int64_t n) {
+    bk::QuantArgs a;
+    a.scale = q.scale;
+    a.col_scale = q.col_scale;
+    a.gsize = q.group_size;
+    a.ngroups = q.group_size > 0 ? (int)cdiv(n, q.group_size) : 1;
+    const int h = 1 << (q.bits - 1);
+    a.qlo = q.alphabet == BAKRON_ALPHABET_ASYMMETRIC ? (float)-h : (float)-(h - 1);
+    a.qhi = (float)(h - 1);
+    return a;
+}
+
 // argument checks shared by the solve entry points (host side, synchronous)
 static bakron_status check_solve_args(bakron_factors* f, const char* who, const float* W, int64_t m,
                                       int64_t n, bakron_quantizer q, const int8_t* codes,
@@ -553,6 +566,14 @@ static bakron_status check_solve_args(bakron_factors* f, const char* who, const 
     }
     if (q.bits < 2 || q.bits > 8) {
         f->err = std::string(who) + ": bits must be in [2, 8]";
+        return BAKRON_EINVAL;
+    }
+    if (q.alphabet != BAKRON_ALPHABET_SYMMETRIC && q.alphabet != BAKRON_ALPHABET_ASYMMETRIC) {
+        f->err = std::string(who) + ": unknown alphabet";
+        return BAKRON_EINVAL;
+    }
+    if (q.group_size < 0) {
+        f->err = std::string(who) + ": group_size must be >= 0";
         return BAKRON_EINVAL;
     }
     if ((m + bk::TS) * (n + bk::TS) > ((int64_t)1 << 40)) {
@@ -573,7 +594,7 @@ static bakron_status solve_impl(const float* W, int64_t m, int64_t n, const bakr
     st = ensure_workspace(f, m, n);
     if (st != BAKRON_OK) return st;
     const int mt = (int)cdiv(m, bk::TS), nt = (int)cdiv(n, bk::TS);
-    const float qmax = (float)((1 << (q.bits - 1)) - 1);
+    const bk::QuantArgs qa = quant_args(q, n);
     // the legacy default stream synchronises implicitly with the (blocking)
     // CU-restricted streams, so calls on it use the one-stream plan
     const bool legacy = stream == nullptr || stream == hipStreamLegacy;
@@ -602,7 +623,7 @@ static bakron_status solve_impl(const float* W, int64_t m, int64_t n, const bakr
     }
     if (e == hipSuccess)
         e = bk::run_plan(ms, f->side, f->plan[pi], W, m, n, mt, nt, f->ws, f->LA, f->LB, f->b_ident,
-                         q.scale, qmax, codes, V, pre, f->knear, f->items, tim, f->ev_rel.data(),
+                         qa, codes, V, pre, f->knear, f->items, tim, f->ev_rel.data(),
                          f->ev_side.data());
     if (fork && e == hipSuccess) {
         e = hipEventRecord(f->ev_join, ms);
@@ -654,9 +675,8 @@ extern "C" bakron_status bakron_solve_antidiag(const float* W, int64_t m, int64_
         f->ad_m = m;
         f->ad_n = n;
     }
-    const float qmax = (float)((1 << (q.bits - 1)) - 1);
     hipError_t e = bk::run_antidiag(stream, W, m, n, f->ad_mem, f->ad_mem + (size_t)cdiv(m * n, 64) * 64, f->LA,
-                                    f->LB, q.scale, qmax, codes, V, pre);
+                                    f->LB, quant_args(q, n), codes, V, pre);
     if (e != hipSuccess) return hip_fail(&f->err, e, "bakron_solve_antidiag: launch");
     return BAKRON_OK;
 }

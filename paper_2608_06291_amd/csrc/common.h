@@ -95,6 +95,45 @@ constexpr int SEG_GRID = 256;
 // J0 of the MT x MT macro tile, z = (first source tile << 1) | push kind
 // (0 column push, 1 row push), w = end of the source tile range.
 
+// Quantiser of a solve (Sec. 3.1): alphabet {qlo..qhi}; scale of entry (i, j)
+// = (gsize > 0 ? scale[i * ngroups + j / gsize] : scale[i]) * col_scale[j]
+// (col_scale null: 1), one fp32 product.  Entries outside the m x n matrix
+// (tile padding) get scale 0: their alphabet is {0} and, since W is zero
+// padded and no feedback reaches them, their error is 0.
+struct QuantArgs {
+    const float* scale;
+    const float* col_scale;
+    int gsize, ngroups;
+    float qlo, qhi;
+};
+
+__device__ inline float entry_scale(const QuantArgs& q, int64_t row, int64_t col, int64_t m,
+                                    int64_t n) {
+    if (row >= m || col >= n) return 0.0f;
+    const float base = q.gsize > 0 ? q.scale[row * q.ngroups + col / q.gsize] : q.scale[row];
+    return q.col_scale ? base * q.col_scale[col] : base;
+}
+
+// The column part of entry_scale for a fixed column: scale index
+// row * rstride + goff, times cf (0 for a padding column).
+struct ColScale {
+    int goff;
+    float cf;
+};
+__device__ inline ColScale col_scale_of(const QuantArgs& q, int64_t col, int64_t n) {
+    ColScale c;
+    c.goff = q.gsize > 0 && col < n ? (int)(col / q.gsize) : 0;
+    c.cf = col >= n ? 0.0f : (q.col_scale ? q.col_scale[col] : 1.0f);
+    return c;
+}
+template <bool GQ>
+__device__ inline float row_scale_of(const QuantArgs& q, int64_t row, const ColScale& c,
+                                     int64_t m) {
+    if (row >= m) return 0.0f;
+    if (!GQ) return q.scale[row];   // per-row scales: c is {0, 1}
+    return q.scale[row * (q.gsize > 0 ? q.ngroups : 1) + c.goff] * c.cf;
+}
+
 // Records the message returned by bakron_last_error() for this thread.
 void set_last_error(const char* msg);
 

@@ -49,8 +49,7 @@ struct SegArgs {
     const float* LA;  // packed factor tiles
     const float* LB;
     int b_ident;      // B = I (no column feedback)
-    const float* scale;
-    float qmax;
+    QuantArgs q;
     int8_t* codes;
     float* V;
     float* pre;       // may be null
@@ -159,6 +158,9 @@ constexpr int PULL_T0 = 2;        // first loop turn whose idle waves may consum
 // L^B[p][i] * E[i][q] and row pushes F[p][j] * L^A[q][j] of both diagonals to
 // both of its entries.  Coefficients are register-resident, each factor row
 // rotated so that step d reads register (d mod 32).
+// GQ: scales per column group and/or per column (else one scale per row, the
+// same for both entries of a thread).
+template <bool GQ>
 __global__ __launch_bounds__(512) void k_seg(SegArgs a) {
     __shared__ float LBt[TS][TS];            // unpadded: the rotated reads below are conflict-free
     __shared__ float LAt[TS][TS];
@@ -180,7 +182,7 @@ __global__ __launch_bounds__(512) void k_seg(SegArgs a) {
     const int c0 = 4 * w + 2 * hf;
     const int q0 = (c0 - p) & 31;
     const int q1 = (q0 + 1) & 31;
-    const float qmax = a.qmax;
+    const float qlo = a.q.qlo, qhi = a.q.qhi;
     const int knear = a.knear;
     const bool roww = w < 4;   // wave-uniform: row-kind or column-kind pull blocks
 
@@ -212,7 +214,10 @@ __global__ __launch_bounds__(512) void k_seg(SegArgs a) {
 
         // inputs of the first tile; later tiles' inputs are prefetched during
         // the previous tile's rounding loop
-        float pf_lb0, pf_lb1, pf_h0, pf_h1, pf_g0, pf_g1, pf_s;
+        float pf_lb0, pf_lb1, pf_h0, pf_h1, pf_g0, pf_g1, pf_s0, pf_s1;
+        // the column part of the scales of the thread's two columns (fixed per strip)
+        const ColScale cs0 = GQ ? col_scale_of(a.q, (int64_t)J * TS + q0, a.n) : ColScale{0, 1.0f};
+        const ColScale cs1 = GQ ? col_scale_of(a.q, (int64_t)J * TS + q1, a.n) : cs0;
         {
             const int64_t tb = ws_tile_offset(I_first, J, a.nt);
             const float* lbp = a.LB + packed_tile_offset(I_first, I_first);
@@ -223,7 +228,8 @@ __global__ __launch_bounds__(512) void k_seg(SegArgs a) {
             pf_g0 = a.Y[tb + p * TS + q0];
             pf_g1 = a.Y[tb + p * TS + q1];
             const int row = I_first * TS + p;
-            pf_s = row < a.m ? a.scale[row] : 0.0f;
+            pf_s0 = row_scale_of<GQ>(a.q, row, cs0, a.m);
+            pf_s1 = GQ ? row_scale_of<GQ>(a.q, row, cs1, a.m) : pf_s0;
         }
 
         // pull state of the next tile (uniform): which operands are staged,
@@ -260,8 +266,9 @@ __global__ __launch_bounds__(512) void k_seg(SegArgs a) {
             float h0 = pf_h0, h1 = pf_h1;
             float g0 = pf_g0, g1 = pf_g1;
             const int row = I * TS + p;
-            const float s = pf_s;
-            const float inv_s = (s > 0.0f) ? 1.0f / s : 0.0f;
+            const float s0 = pf_s0, s1 = pf_s1;   // scales of the thread's two entries
+            const float inv_s0 = (s0 > 0.0f) ? 1.0f / s0 : 0.0f;
+            const float inv_s1 = (s1 > 0.0f) ? 1.0f / s1 : 0.0f;
             const int kc = a.b_ident ? 0 : (knear < I ? knear : I);   // column sources k = 1..kc
 
             // multiplies source distance k of tile It into pacc (row or column kind)
@@ -361,7 +368,8 @@ __global__ __launch_bounds__(512) void k_seg(SegArgs a) {
                 pf_g0 = a.Y[tb + p * TS + q0];
                 pf_g1 = a.Y[tb + p * TS + q1];
                 const int rn = In * TS + p;
-                pf_s = rn < a.m ? a.scale[rn] : 0.0f;
+                pf_s0 = row_scale_of<GQ>(a.q, rn, cs0, a.m);
+                pf_s1 = GQ ? row_scale_of<GQ>(a.q, rn, cs1, a.m) : pf_s0;
             }
 
             float lbr[TS], lar0[TS], lar1[TS];
@@ -369,7 +377,7 @@ __global__ __launch_bounds__(512) void k_seg(SegArgs a) {
             for (int k = 0; k < TS; ++k) { lbr[k] = LBt[p][(k - q0) & 31]; lar0[k] = LAt[q0][(k - p) & 31]; lar1[k] = LAt[q1][(k - p) & 31]; }
 
             // 2. in-tile rounding.  Quantisation without branches: a zero scale
-            // gives inv_s = 0, so x = 0, code 0, V = 0 and E = -W~ (the row's
+            // gives inv_s = 0, so x = 0, code 0, V = 0 and E = -W~ (the entry's
             // alphabet is {0}).  Each thread keeps E, F and x of its own two
             // entries when it processes them.
             float eo0 = 0.0f, eo1 = 0.0f, fo0 = 0.0f, fo1 = 0.0f, xv0 = 0.0f, xv1 = 0.0f;
@@ -380,9 +388,9 @@ __global__ __launch_bounds__(512) void k_seg(SegArgs a) {
                 // slot 0: anti-diagonal d
                 const bool v0 = act && (p + q0 == d);
                 const float acc0 = g0 + h0;
-                const float x0 = acc0 * inv_s;
-                const float r0 = __builtin_amdgcn_fmed3f(rintf(x0), -qmax, qmax);
-                const float ew0 = fmaf(r0, s, -acc0);
+                const float x0 = acc0 * inv_s0;
+                const float r0 = __builtin_amdgcn_fmed3f(rintf(x0), qlo, qhi);
+                const float ew0 = fmaf(r0, s0, -acc0);
                 const float e0 = v0 ? ew0 : 0.0f;
                 const float f0 = v0 ? g0 + ew0 : 0.0f;
                 // slot 1: anti-diagonal d + 1, plus the two pushes from d
@@ -392,9 +400,9 @@ __global__ __launch_bounds__(512) void k_seg(SegArgs a) {
                 const float h1n = fmaf(f0, lar1[kp & 31], h1);
                 const bool v1 = act && (p + q1 == d + 1);
                 const float acc1 = g1n + h1n;
-                const float x1 = acc1 * inv_s;
-                const float r1 = __builtin_amdgcn_fmed3f(rintf(x1), -qmax, qmax);
-                const float ew1 = fmaf(r1, s, -acc1);
+                const float x1 = acc1 * inv_s1;
+                const float r1 = __builtin_amdgcn_fmed3f(rintf(x1), qlo, qhi);
+                const float ew1 = fmaf(r1, s1, -acc1);
                 const float e1 = v1 ? ew1 : 0.0f;
                 const float f1 = v1 ? g1n + ew1 : 0.0f;
                 // broadcast (the inactive half writes the dummy slots)
@@ -474,22 +482,22 @@ __global__ __launch_bounds__(512) void k_seg(SegArgs a) {
             if (tid == 0)
                 __hip_atomic_store(a.flags + I * a.nt + J, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 
-            const int64_t col0 = (int64_t)J * TS + q0, col1 = (int64_t)J * TS + q1;
             const float nan = __builtin_nanf("");
+            const int64_t col0 = (int64_t)J * TS + q0, col1 = (int64_t)J * TS + q1;
             if (row < a.m) {
                 if (col0 < a.n) {
                     const int64_t o = (int64_t)row * a.n + col0;
-                    const float r = __builtin_amdgcn_fmed3f(rintf(xv0), -qmax, qmax);
+                    const float r = __builtin_amdgcn_fmed3f(rintf(xv0), qlo, qhi);
                     a.codes[o] = (int8_t)(int)r;
-                    a.V[o] = r * s;
-                    if (a.pre) a.pre[o] = s > 0.0f ? xv0 : nan;
+                    a.V[o] = r * s0;
+                    if (a.pre) a.pre[o] = s0 > 0.0f ? xv0 : nan;
                 }
                 if (col1 < a.n) {
                     const int64_t o = (int64_t)row * a.n + col1;
-                    const float r = __builtin_amdgcn_fmed3f(rintf(xv1), -qmax, qmax);
+                    const float r = __builtin_amdgcn_fmed3f(rintf(xv1), qlo, qhi);
                     a.codes[o] = (int8_t)(int)r;
-                    a.V[o] = r * s;
-                    if (a.pre) a.pre[o] = s > 0.0f ? xv1 : nan;
+                    a.V[o] = r * s1;
+                    if (a.pre) a.pre[o] = s1 > 0.0f ? xv1 : nan;
                 }
             }
         }
@@ -698,7 +706,7 @@ __global__ __launch_bounds__(256) void k_prep(const float* __restrict__ W, int64
 // pair around every launch, in enqueue order (prep first).
 hipError_t run_plan(hipStream_t st, hipStream_t side, const Plan& plan, const float* W, int64_t m,
                     int64_t n, int mt, int nt, const Workspace& ws, const float* LA, const float* LB,
-                    int b_ident, const float* scale, float qmax, int8_t* codes, float* V, float* pre,
+                    int b_ident, const QuantArgs& q, int8_t* codes, float* V, float* pre,
                     int knear, const int4* items, hipEvent_t* tim, hipEvent_t* ev_rel,
                     hipEvent_t* ev_side) {
     int ti = 0;
@@ -713,7 +721,7 @@ hipError_t run_plan(hipStream_t st, hipStream_t side, const Plan& plan, const fl
 
     SegArgs sa{};
     sa.mt = mt; sa.nt = nt; sa.m = m; sa.n = n; sa.X = ws.X; sa.Y = ws.Y;
-    sa.LA = LA; sa.LB = LB; sa.b_ident = b_ident; sa.scale = scale; sa.qmax = qmax;
+    sa.LA = LA; sa.LB = LB; sa.b_ident = b_ident; sa.q = q;
     sa.codes = codes; sa.V = V; sa.pre = pre; sa.knear = knear; sa.flags = ws.flags;
     sa.status = ws.status;
     NodeArgs nd{};
@@ -745,7 +753,10 @@ hipError_t run_plan(hipStream_t st, hipStream_t side, const Plan& plan, const fl
                 sa.nstrips = op.nstrips;
                 sa.counter = ws.counters + op.counter;
                 const int grid = op.nstrips < SEG_GRID ? op.nstrips : SEG_GRID;
-                hipLaunchKernelGGL(k_seg, dim3((unsigned)grid), dim3(512), 0, st, sa);
+                if (q.gsize > 0 || q.col_scale)
+                    hipLaunchKernelGGL(k_seg<true>, dim3((unsigned)grid), dim3(512), 0, st, sa);
+                else
+                    hipLaunchKernelGGL(k_seg<false>, dim3((unsigned)grid), dim3(512), 0, st, sa);
             } else {
                 node(op, st);
             }

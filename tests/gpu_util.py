@@ -46,6 +46,23 @@ def knear(k):
             os.environ["BAKRON_KNEAR"] = old
 
 
+def quant_kwargs(p):
+    """Quantiser of a problem dict for the binding: alphabet, group size and
+    per-column factors (absent: the per-row symmetric quantiser)."""
+    import torch
+    kw = dict(alphabet=p.get("alphabet", "sym"), group_size=p.get("group_size", 0))
+    if p.get("col_scale") is not None:
+        kw["col_scale"] = torch.from_numpy(np.ascontiguousarray(p["col_scale"], np.float32)).to("cuda:0")
+    return kw
+
+
+def oracle_scales(p, oracle):
+    """Per-entry scales of the problem's quantiser (m x n, fp32 values)."""
+    m, n = p["W"].shape
+    return oracle.entry_scales(p["scale"], m, n, group_size=p.get("group_size", 0),
+                               col_scale=p.get("col_scale"))
+
+
 def gpu_run(p, debug=True, k=None, repeat=1):
     """Factor + solve on cuda:0; returns numpy codes, V, pre (pre None if not debug)."""
     import torch
@@ -55,15 +72,20 @@ def gpu_run(p, debug=True, k=None, repeat=1):
     B = None if p["B"] is None else torch.from_numpy(np.ascontiguousarray(p["B"], np.float32)).to(dev)
     W = torch.from_numpy(np.ascontiguousarray(p["W"], np.float32)).to(dev)
     s = torch.from_numpy(np.ascontiguousarray(p["scale"], np.float32)).to(dev)
+    qk = quant_kwargs(p)
     with knear(k):
-        f = pk.factor(A, B, p["damp"])
+        if p.get("B_blocks") is not None:
+            Bb = torch.from_numpy(np.ascontiguousarray(p["B_blocks"], np.float32)).to(dev)
+            f = pk.factor_blockdiag(A, Bb, p["damp"])
+        else:
+            f = pk.factor(A, B, p["damp"])
     outs = []
     for _ in range(repeat):
         # poison outputs so unwritten entries cannot pass
         codes = torch.full(W.shape, 100, dtype=torch.int8, device=dev)
         V = torch.full(W.shape, float("nan"), dtype=torch.float32, device=dev)
         pre = torch.full(W.shape, float("nan"), dtype=torch.float32, device=dev) if debug else None
-        r = pk.solve(W, f, p["bits"], s, codes=codes, V=V, pre=pre, debug=debug)
+        r = pk.solve(W, f, p["bits"], s, codes=codes, V=V, pre=pre, debug=debug, **qk)
         torch.cuda.synchronize()
         assert f.check(), "a tile-ordering wait of the solve gave up"
         outs.append(tuple(None if t is None else t.cpu().numpy() for t in
@@ -73,8 +95,11 @@ def gpu_run(p, debug=True, k=None, repeat=1):
 
 
 def v_is_scale_times_code(V, codes, scale):
-    """V_ij must be the single fp32 product s_i * c_ij."""
-    ref = (scale.astype(np.float32)[:, None] * codes.astype(np.float32)).astype(np.float32)
+    """V_ij must be the single fp32 product s_ij * c_ij (scale: per row or
+    per entry)."""
+    S = np.asarray(scale, np.float32)
+    S = S[:, None] if S.ndim == 1 else S
+    ref = (S * codes.astype(np.float32)).astype(np.float32)
     return np.array_equal(V.view(np.uint32), ref.view(np.uint32)) or np.array_equal(V, ref)
 
 
@@ -82,11 +107,17 @@ def check_against_oracle(p, codes, V, pre, oracle, label=""):
     """Full element-by-element comparison with the tie-forced oracle replay."""
     m, n = p["W"].shape
     assert codes.dtype == np.int8 and codes.shape == (m, n)
-    l = (1 << (p["bits"] - 1)) - 1
-    assert np.all(np.abs(codes.astype(np.int32)) <= l), f"{label}: code outside alphabet"
-    assert v_is_scale_times_code(V, codes, p["scale"]), f"{label}: V != s*c"
-    forced = oracle.solve(p["W"], p["A"], p["B"], p["damp"], p["scale"], p["bits"],
-                          forced=codes, tie_window=TIE_WINDOW)
+    alphabet = p.get("alphabet", "sym")
+    lo, hi = oracle.alphabet_bounds(p["bits"], alphabet)
+    assert np.all((codes.astype(np.int32) >= lo) & (codes.astype(np.int32) <= hi)), \
+        f"{label}: code outside alphabet"
+    S = oracle_scales(p, oracle)
+    assert v_is_scale_times_code(V, codes, S), f"{label}: V != s*c"
+    B = p["B"]
+    if p.get("B_blocks") is not None:
+        B = block_diag(p["B_blocks"])
+    forced = oracle.solve(p["W"], p["A"], B, p["damp"], S, p["bits"],
+                          forced=codes, tie_window=TIE_WINDOW, alphabet=alphabet)
     viol = int(np.count_nonzero(forced["codes"] != codes))
     flips = forced["n_flip"]
     res = dict(violations=viol, flips=flips, excused=forced["n_excused"], total=m * n)
@@ -94,12 +125,12 @@ def check_against_oracle(p, codes, V, pre, oracle, label=""):
         fin = np.isfinite(forced["pre"])
         res["margin"] = float(np.max(np.abs(pre[fin].astype(np.float64) - forced["pre"][fin]))) \
             if fin.any() else 0.0
-    og = oracle.objective(p["W"], V.astype(np.float64), p["A"], p["B"], p["damp"])
-    oo = oracle.objective(p["W"], forced["V"], p["A"], p["B"], p["damp"])
+    og = oracle.objective(p["W"], V.astype(np.float64), p["A"], B, p["damp"])
+    oo = oracle.objective(p["W"], forced["V"], p["A"], B, p["damp"])
     # The GPU returns V in fp32 (|dV| <= 2^-24 |V| per entry), so the two
     # objectives can differ by up to 2 eps sqrt(obj(D) obj(V)) + eps^2 obj(V)
     # with obj(V) = tr(V^T B V A); this floor matters only when V ~ W.
-    ov = oracle.objective(np.zeros_like(forced["V"]), forced["V"], p["A"], p["B"], p["damp"])
+    ov = oracle.objective(np.zeros_like(forced["V"]), forced["V"], p["A"], B, p["damp"])
     eps = 2.0 ** -24
     floor = 2 * eps * np.sqrt(abs(oo) * abs(ov)) + eps * eps * abs(ov)
     res["obj_rel"] = max(abs(og - oo) - floor, 0.0) / max(abs(oo), 1e-300)
@@ -109,9 +140,19 @@ def check_against_oracle(p, codes, V, pre, oracle, label=""):
     assert res["obj_rel"] <= OBJ_RTOL, f"{label}: objective rel diff {res['obj_rel']}"
     if flips == 0:
         # forcing changed nothing, so the free-running oracle must agree exactly
-        free = oracle.solve(p["W"], p["A"], p["B"], p["damp"], p["scale"], p["bits"])
+        free = oracle.solve(p["W"], p["A"], B, p["damp"], S, p["bits"], alphabet=alphabet)
         assert np.array_equal(free["codes"], codes), f"{label}: free-running mismatch"
     return res
+
+
+def block_diag(blocks):
+    """The m x m block-diagonal matrix of nblocks x hb x hb blocks (fp32)."""
+    blocks = np.asarray(blocks, np.float32)
+    nb, hb, _ = blocks.shape
+    out = np.zeros((nb * hb, nb * hb), np.float32)
+    for h in range(nb):
+        out[h * hb:(h + 1) * hb, h * hb:(h + 1) * hb] = blocks[h]
+    return out
 
 
 def gpu_run_antidiag(p):
@@ -127,7 +168,7 @@ def gpu_run_antidiag(p):
     codes = torch.full(W.shape, 100, dtype=torch.int8, device=dev)
     V = torch.full(W.shape, float("nan"), dtype=torch.float32, device=dev)
     pre = torch.full(W.shape, float("nan"), dtype=torch.float32, device=dev)
-    pk.solve_antidiag(W, f, p["bits"], s, codes=codes, V=V, pre=pre)
+    pk.solve_antidiag(W, f, p["bits"], s, codes=codes, V=V, pre=pre, **quant_kwargs(p))
     torch.cuda.synchronize()
     out = (codes.cpu().numpy(), V.cpu().numpy(), pre.cpu().numpy())
     f.close()

@@ -120,3 +120,33 @@ def test_factor_construction_host_validation(lib):
                   None) == pk.BAKRON_EINVAL
     assert lib.bakron_sample_weights(None, 10, 4, None, one, None) == pk.BAKRON_EINVAL
     assert lib.bakron_sample_weights(one, -2, 4, None, one, None) == pk.BAKRON_EINVAL
+
+
+def test_quantiser_and_scale_search_host_validation(lib):
+    import paper_2608_06291_amd as pk
+    one = ctypes.c_void_p(256)
+    sc = ctypes.c_void_p(0)
+    # the MSE search: bad bits / alphabet / grid / shrink / sizes
+    for args in ((one, 4, 8, 1, 0, 0, 100, 0.5), (one, 4, 8, 4, 2, 0, 100, 0.5),
+                 (one, 4, 8, 4, 0, -1, 100, 0.5), (one, 4, 8, 4, 0, 0, 256, 0.5),
+                 (one, 4, 8, 4, 0, 0, 100, 1.0), (one, 0, 8, 4, 0, 0, 100, 0.5),
+                 (None, 4, 8, 4, 0, 0, 100, 0.5)):
+        assert lib.bakron_mse_scales(*args, one, None) == pk.BAKRON_EINVAL, args
+    assert lib.bakron_mse_scales(one, 4, 8, 4, 0, 0, 100, 0.5, None, None) == pk.BAKRON_EINVAL
+    # block-diagonal factor: bad block arguments
+    h = ctypes.c_void_p(0)
+    assert lib.bakron_factor_blockdiag(one, 8, None, 2, 4, 0.01, None,
+                                       ctypes.byref(h)) == pk.BAKRON_EINVAL
+    assert lib.bakron_factor_blockdiag(one, 8, one, 0, 4, 0.01, None,
+                                       ctypes.byref(h)) == pk.BAKRON_EINVAL
+    assert b"block" in lib.bakron_last_error()
+    del sc
+
+
+def test_binding_checks_quantiser_shapes():
+    import torch
+    import paper_2608_06291_amd as pk
+    with pytest.raises(TypeError):   # CPU tensors are refused before any shape logic
+        pk.mse_scales(torch.zeros(4, 4), 3)
+    with pytest.raises((TypeError, ValueError)):
+        pk._lib._quantizer(3, torch.zeros(4), 4, 8, "sym", 0, None)
