@@ -357,6 +357,40 @@ bakron_status bakron_mlp_local_factors(const float *x, const float *g, const flo
                                        int64_t dm, int64_t dff, int32_t style, float *A, float *B,
                                        void *work, size_t *work_bytes, hipStream_t stream);
 
+/*
+ * bakron_quadform_weights -- w_k = x_k^T M x_k for every sample (row) x_k of
+ * X: the per-sample weights tr(b^T B^(i) b) of the later Shampoo power steps
+ * (App. A: A^(i+1) = E[tr(b^T B^(i) b) a a^T]).
+ *   X  device, N x d;  M  device, d x d, SYMMETRIC (M_tj is read as M_jt);
+ *   w  device, N outputs.  0 <= d <= 2^17.
+ * Two launches (X M on fp32 MFMA with the row sums fused, then the sum over
+ * column blocks in a fixed order).  Workspace as above: ceil(d / 128) * N
+ * floats.
+ */
+bakron_status bakron_quadform_weights(const float *X, int64_t N, int64_t d, const float *M,
+                                      float *w, void *work, size_t *work_bytes, hipStream_t stream);
+
+/*
+ * bakron_kron_factors_iter, bakron_mlp_local_factors_iter -- the Shampoo-style
+ * factors after `iters` unnormalised power steps on the rearranged Hessian
+ * from A^(0) = I, B^(0) = I (App. A; iters = 1 is BAKRON_SHAMPOO):
+ *   A^(i+1) = E[tr(b^T B^(i) b) a a^T],   B^(i+1) = E[tr(a^T A^(i) a) b b^T]
+ * with, in the MLP-local case (b = D_g W_down^T, D = W_down),
+ *   tr(b^T X b) = g^T (X (.) D^T D) g,   b b^T = (g g^T) (.) D^T D.
+ * Each step is one more pass over the calibration samples.  The iterates are
+ * not normalised (the rounding is invariant to scaling A or B); their size
+ * grows geometrically with iters, so keep iters small (<= 64 accepted).
+ * Arguments otherwise as bakron_kron_factors / bakron_mlp_local_factors; the
+ * MLP-local workspace holds one more dff x dff matrix when iters > 1.
+ */
+bakron_status bakron_kron_factors_iter(const float *a, const float *b, int64_t N, int64_t n,
+                                       int64_t m, int32_t iters, float *A, float *B, void *work,
+                                       size_t *work_bytes, hipStream_t stream);
+bakron_status bakron_mlp_local_factors_iter(const float *x, const float *g, const float *D,
+                                            int64_t N, int64_t dm, int64_t dff, int32_t iters,
+                                            float *A, float *B, void *work, size_t *work_bytes,
+                                            hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -19,7 +19,8 @@ EXPORTED = ("bakron_factor", "bakron_solve", "bakron_solve_debug", "bakron_facto
             "bakron_factor_export", "bakron_profile_enable", "bakron_profile_read",
             "bakron_solve_check", "bakron_solve_antidiag", "bakron_gram",
             "bakron_sample_weights", "bakron_kron_factors", "bakron_mlp_local_factors",
-            "bakron_mse_scales", "bakron_factor_blockdiag")
+            "bakron_mse_scales", "bakron_factor_blockdiag", "bakron_quadform_weights",
+            "bakron_kron_factors_iter", "bakron_mlp_local_factors_iter")
 
 ALPHABETS = {"sym": 0, "asym": 1}
 
@@ -98,6 +99,14 @@ def load(path: str = LIB_PATH):
     lib.bakron_sample_weights.argtypes = [vp, i64, i64, vp, vp, vp]
     lib.bakron_kron_factors.restype = ctypes.c_int
     lib.bakron_kron_factors.argtypes = [vp, vp, i64, i64, i64, ctypes.c_int32, vp, vp, vp, szp, vp]
+    lib.bakron_quadform_weights.restype = ctypes.c_int
+    lib.bakron_quadform_weights.argtypes = [vp, i64, i64, vp, vp, vp, szp, vp]
+    lib.bakron_kron_factors_iter.restype = ctypes.c_int
+    lib.bakron_kron_factors_iter.argtypes = [vp, vp, i64, i64, i64, ctypes.c_int32, vp, vp, vp,
+                                             szp, vp]
+    lib.bakron_mlp_local_factors_iter.restype = ctypes.c_int
+    lib.bakron_mlp_local_factors_iter.argtypes = [vp, vp, vp, i64, i64, i64, ctypes.c_int32, vp,
+                                                  vp, vp, szp, vp]
     lib.bakron_mlp_local_factors.restype = ctypes.c_int
     lib.bakron_mlp_local_factors.argtypes = [vp, vp, vp, i64, i64, i64, ctypes.c_int32, vp, vp, vp,
                                              szp, vp]
@@ -416,8 +425,27 @@ def sample_weights(X, c=None, w=None):
     return w
 
 
-def kron_factors(a, b, style: str = "kfac"):
-    """bakron_kron_factors: (A, B) of a global Hessian from paired vector
+def quadform_weights(X, M, w=None):
+    """bakron_quadform_weights: w_k = x_k^T M x_k (M symmetric) on the current stream."""
+    import torch
+    lib = load()
+    _check_dev(X, "X", torch.float32)
+    _check_dev(M, "M", torch.float32)
+    N, d = X.shape
+    if tuple(M.shape) != (d, d):
+        raise ValueError("M must be d x d")
+    if w is None:
+        w = torch.empty((N,), dtype=torch.float32, device=X.device)
+    _check_dev(w, "w", torch.float32)
+    st = _stream(torch, X.device)
+    _with_workspace(lambda wk, nb: lib.bakron_quadform_weights(_ptr(X), N, d, _ptr(M), _ptr(w), wk,
+                                                               nb, st), X.device)
+    return w
+
+
+def kron_factors(a, b, style: str = "kfac", iters: int = 1):
+    """bakron_kron_factors (iters = 1) or bakron_kron_factors_iter (Shampoo
+    with `iters` power steps): (A, B) of a global Hessian from paired vector
     samples a (N x n) and b (N x m) on the current stream."""
     import torch
     lib = load()
@@ -430,12 +458,18 @@ def kron_factors(a, b, style: str = "kfac"):
     A = torch.empty((n, n), dtype=torch.float32, device=a.device)
     B = torch.empty((m, m), dtype=torch.float32, device=a.device)
     st = _stream(torch, a.device)
+    if iters != 1:
+        if style != "shampoo":
+            raise ValueError("power steps need style='shampoo'")
+        _with_workspace(lambda wk, nb: lib.bakron_kron_factors_iter(
+            _ptr(a), _ptr(b), N, n, m, int(iters), _ptr(A), _ptr(B), wk, nb, st), a.device)
+        return A, B
     _with_workspace(lambda wk, nb: lib.bakron_kron_factors(_ptr(a), _ptr(b), N, n, m, STYLES[style],
                                                            _ptr(A), _ptr(B), wk, nb, st), a.device)
     return A, B
 
 
-def mlp_local_factors(x, g, D, style: str = "kfac"):
+def mlp_local_factors(x, g, D, style: str = "kfac", iters: int = 1):
     """bakron_mlp_local_factors: (A, B) of the MLP-local Hessian from inputs x
     (N x dm), features g or f (N x dff) and W_down D (dm x dff)."""
     import torch
@@ -449,6 +483,13 @@ def mlp_local_factors(x, g, D, style: str = "kfac"):
     A = torch.empty((dm, dm), dtype=torch.float32, device=x.device)
     B = torch.empty((dff, dff), dtype=torch.float32, device=x.device)
     st = _stream(torch, x.device)
+    if iters != 1:
+        if style != "shampoo":
+            raise ValueError("power steps need style='shampoo'")
+        _with_workspace(lambda wk, nb: lib.bakron_mlp_local_factors_iter(
+            _ptr(x), _ptr(g), _ptr(D), N, dm, dff, int(iters), _ptr(A), _ptr(B), wk, nb, st),
+            x.device)
+        return A, B
     _with_workspace(lambda wk, nb: lib.bakron_mlp_local_factors(_ptr(x), _ptr(g), _ptr(D), N, dm,
                                                                 dff, STYLES[style], _ptr(A),
                                                                 _ptr(B), wk, nb, st), x.device)

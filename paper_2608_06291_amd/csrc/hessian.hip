@@ -365,6 +365,170 @@ static hipError_t run_gram(hipStream_t st, const GramGeom& g, const float* X, in
     return hipGetLastError();
 }
 
+// ----------------------------------------------------------------------------
+// Per-sample quadratic forms w_k = x_k^T M x_k (M symmetric d x d): the
+// weights tr(b^T B b) of the later Shampoo power steps (App. A).  Workgroup
+// (row block R, column block J) computes the 128 x 128 tile of Y = X M
+// (Y_kj = sum_t X_kt M_jt, M symmetric) on fp32 MFMA, then
+// part[J][k] = sum_{j in J} Y_kj X_kj.  Both operands are rows with the
+// inner index contiguous, staged as 16-byte copies (thread t: row t >> 1,
+// inner quarter-chunk 16 (t & 1)).  k_quadform_reduce adds the column blocks
+// in order.
+struct QuadArgs {
+    const float* X;
+    int64_t N, d;
+    const float* M;
+    int nJ;
+    float* part;   // [nJ][N]
+};
+
+template <bool VEC>
+__global__ __launch_bounds__(256, 2) void k_quadform(QuadArgs a) {
+    __shared__ __attribute__((aligned(16))) float As[2][GB][GSTR];
+    __shared__ __attribute__((aligned(16))) float Bs[2][GB][GSTR];
+    __shared__ float red[2][GB];
+    const int J = (int)(blockIdx.x % (unsigned)a.nJ);
+    const int64_t R = blockIdx.x / (unsigned)a.nJ;
+    const int64_t k0 = R * GB, j0 = (int64_t)J * GB;
+    const int64_t d = a.d;
+    const int tid = threadIdx.x;
+    const int wv = tid >> 6, l = tid & 63;
+    const int wm = wv >> 1, wn = wv & 1;
+    const int lr = l & 31, lk = l >> 5;
+    const int srow = tid >> 1, sq = 16 * (tid & 1);
+    const bool arow_in = k0 + srow < a.N, brow_in = j0 + srow < d;
+    const float* xa = a.X + (arow_in ? k0 + srow : 0) * d;
+    const float* mb = a.M + (brow_in ? j0 + srow : 0) * d;
+    f32x4 ra[4], rb[4];
+    int64_t tbase = 0;
+    auto load = [&](int64_t t0) {
+        tbase = t0;
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            const int64_t t = t0 + sq + 4 * v;
+            if (VEC) {
+                const int64_t tc = t < d ? t : 0;   // d % 4 == 0: a whole chunk is in or out
+                ra[v] = *reinterpret_cast<const f32x4*>(xa + tc);
+                rb[v] = *reinterpret_cast<const f32x4*>(mb + tc);
+            } else {
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    const int64_t tc = t + u < d ? t + u : 0;
+                    ra[v][u] = xa[tc];
+                    rb[v][u] = mb[tc];
+                }
+            }
+        }
+    };
+    auto store = [&](int sb) {
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const bool tin = tbase + sq + 4 * v + u < d;
+                ra[v][u] = (tin && arow_in) ? ra[v][u] : 0.0f;
+                rb[v][u] = (tin && brow_in) ? rb[v][u] : 0.0f;
+            }
+            *reinterpret_cast<f32x4*>(&As[sb][srow][sq + 4 * v]) = ra[v];
+            *reinterpret_cast<f32x4*>(&Bs[sb][srow][sq + 4 * v]) = rb[v];
+        }
+    };
+    f32x16 acc[2][2];
+#pragma unroll
+    for (int x = 0; x < 2; ++x)
+#pragma unroll
+        for (int y = 0; y < 2; ++y) acc[x][y] = f32x16{0};
+    const int nch = (int)((d + GK - 1) / GK);
+    load(0);
+    store(0);
+    __syncthreads();
+    for (int c = 0; c < nch; ++c) {
+        const int sb = c & 1;
+        const bool more = c + 1 < nch;
+        if (more) load((int64_t)(c + 1) * GK);
+        f32x4 fa[2][4], fb[2][4];
+#pragma unroll
+        for (int x = 0; x < 2; ++x)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                fa[x][v] = *reinterpret_cast<const f32x4*>(&As[sb][(2 * wm + x) * TS + lr][lk * 16 + v * 4]);
+                fb[x][v] = *reinterpret_cast<const f32x4*>(&Bs[sb][(2 * wn + x) * TS + lr][lk * 16 + v * 4]);
+            }
+#pragma unroll
+        for (int st = 0; st < 16; ++st)
+#pragma unroll
+            for (int x = 0; x < 2; ++x)
+#pragma unroll
+                for (int y = 0; y < 2; ++y)
+                    acc[x][y] = __builtin_amdgcn_mfma_f32_32x32x2f32(fa[x][st >> 2][st & 3],
+                                                                    fb[y][st >> 2][st & 3], acc[x][y],
+                                                                    0, 0, 0);
+        if (more) store(sb ^ 1);
+        __syncthreads();
+    }
+    // acc[x][y][r] = Y(row (2wm + x) * 32 + (r >> 2) * 8 + lk * 4 + (r & 3),
+    //                  column (2wn + y) * 32 + lr); row sums of Y (.) X over the
+    // wave's 64 columns, then over the lanes of a row, then over the two waves
+    // that share the rows (wn = 0, 1)
+#pragma unroll
+    for (int x = 0; x < 2; ++x)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            const int row = (2 * wm + x) * TS + (r >> 2) * 8 + lk * 4 + (r & 3);
+            const int64_t k = k0 + row;
+            float v = 0.0f;
+#pragma unroll
+            for (int y = 0; y < 2; ++y) {
+                const int64_t j = j0 + (2 * wn + y) * TS + lr;
+                const float xv = (k < a.N && j < d) ? a.X[k * d + j] : 0.0f;
+                v = fmaf(acc[x][y][r], xv, v);
+            }
+#pragma unroll
+            for (int off = 16; off >= 1; off >>= 1) v += __shfl_xor(v, off, 32);
+            if (lr == 0) red[wn][row] = v;
+        }
+    __syncthreads();
+    if (tid < GB && k0 + tid < a.N) a.part[(int64_t)J * a.N + k0 + tid] = red[0][tid] + red[1][tid];
+}
+
+__global__ __launch_bounds__(256) void k_quadform_reduce(const float* __restrict__ part, int nJ,
+                                                         int64_t N, float* __restrict__ w) {
+    const int64_t k = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (k >= N) return;
+    float s = 0.0f;
+    for (int J = 0; J < nJ; ++J) s += part[(int64_t)J * N + k];
+    w[k] = s;
+}
+
+// C = A (.) B entrywise (n elements); C may alias A or B.
+__global__ __launch_bounds__(256) void k_hadamard(const float* A, const float* B, int64_t n,
+                                                  float* C) {
+    const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (e < n) C[e] = A[e] * B[e];
+}
+
+static size_t quadform_part_bytes(int64_t N, int64_t d) {
+    return (size_t)((d + GB - 1) / GB) * (size_t)std::max<int64_t>(N, 1) * sizeof(float);
+}
+
+static hipError_t run_quadform(hipStream_t st, const float* X, int64_t N, int64_t d, const float* M,
+                               float* w, float* part) {
+    if (N == 0) return hipSuccess;
+    const int nJ = (int)std::max<int64_t>(1, (d + GB - 1) / GB);
+    QuadArgs a{X, N, d, M, nJ, part};
+    const bool vec = d % 4 == 0 && ((uintptr_t)X & 15) == 0 && ((uintptr_t)M & 15) == 0;
+    const dim3 grid((unsigned)(((N + GB - 1) / GB) * nJ));
+    if (vec)
+        hipLaunchKernelGGL(k_quadform<true>, grid, dim3(256), 0, st, a);
+    else
+        hipLaunchKernelGGL(k_quadform<false>, grid, dim3(256), 0, st, a);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k_quadform_reduce, dim3((unsigned)((N + 255) / 256)), dim3(256), 0, st, part,
+                       nJ, N, w);
+    return hipGetLastError();
+}
+
 static int device_cus() {
     int dev = 0, ncu = 0;
     if (hipGetDevice(&dev) != hipSuccess) return 0;
@@ -435,37 +599,154 @@ extern "C" bakron_status bakron_gram(const float* X, int64_t N, int64_t d, const
     return e == hipSuccess ? BAKRON_OK : hess_hip(e, "bakron_gram: launch");
 }
 
-extern "C" bakron_status bakron_kron_factors(const float* a, const float* b, int64_t N, int64_t n,
-                                             int64_t m, int32_t style, float* A, float* B,
-                                             void* work, size_t* work_bytes, hipStream_t stream) {
-    bk::set_last_error("");
-    if (N <= 0 || n <= 0 || m <= 0 || N > HESS_N_MAX || n > HESS_DIM_MAX || m > HESS_DIM_MAX)
-        return hess_fail("bad size");
-    if (style != BAKRON_KFAC && style != BAKRON_SHAMPOO) return hess_fail("bad style");
+// Carves the workspace: [partials | weights x2 | extra], 256-byte aligned.
+struct HessWork {
+    float* part;
+    float* w0;
+    float* w1;
+    float* extra;
+};
+static HessWork carve(void* work, size_t part, size_t wbytes) {
+    char* p = static_cast<char*>(work);
+    HessWork h;
+    h.part = reinterpret_cast<float*>(p);
+    h.w0 = reinterpret_cast<float*>(p + align256(part));
+    h.w1 = reinterpret_cast<float*>(p + align256(part) + wbytes);
+    h.extra = reinterpret_cast<float*>(p + align256(part) + 2 * wbytes);
+    return h;
+}
+
+// Global (vector) case, App. A: K-FAC, or `iters` unnormalised power steps
+// from (I, I).  Step 1 weighs by |b_k|^2 and |a_k|^2; step i > 1 by
+// b_k^T B^(i-1) b_k and a_k^T A^(i-1) a_k, after which A and B are
+// overwritten in place (the previous pair is no longer needed).
+static bakron_status kron_factors_impl(const char* who, const float* a, const float* b, int64_t N,
+                                       int64_t n, int64_t m, bool shampoo, int iters, float* A,
+                                       float* B, void* work, size_t* work_bytes,
+                                       hipStream_t stream) {
+    if (N <= 0 || n <= 0 || m <= 0 || N > HESS_N_MAX || n > HESS_DIM_MAX || m > HESS_DIM_MAX ||
+        iters < 1 || iters > 64)
+        return hess_fail("bad size or iteration count");
+    if (iters > 1 && ((N + bk::GB - 1) / bk::GB) * ((std::max(n, m) + bk::GB - 1) / bk::GB) >
+                         ((int64_t)1 << 31) - 1)
+        return hess_fail("too many samples for the power steps");
     const int ncu = bk::device_cus();
     const GramGeom ga = bk::gram_geom(N, n, ncu), gb = bk::gram_geom(N, m, ncu);
-    const size_t part = std::max(bk::gram_part_bytes(ga), bk::gram_part_bytes(gb));
-    const size_t wbytes = style == BAKRON_SHAMPOO ? align256((size_t)N * sizeof(float)) : 0;
+    size_t part = std::max(bk::gram_part_bytes(ga), bk::gram_part_bytes(gb));
+    if (iters > 1)
+        part = std::max({part, bk::quadform_part_bytes(N, n), bk::quadform_part_bytes(N, m)});
+    const size_t wbytes = shampoo ? align256((size_t)N * sizeof(float)) : 0;
     bool query;
     bakron_status st = workspace_check(work, work_bytes, align256(part) + 2 * wbytes, &query);
     if (st != BAKRON_OK || query) return st;
     if (!a || !b || !A || !B) return hess_fail("null pointer");
-    float* P = static_cast<float*>(work);
-    float* wa = nullptr;   // |a_k|^2, weights of B
-    float* wb = nullptr;   // |b_k|^2, weights of A
+    const HessWork h = carve(work, part, wbytes);
     const float inv = (float)(1.0 / (double)N);
+    float* wa = shampoo ? h.w0 : nullptr;   // weights of B (from a)
+    float* wb = shampoo ? h.w1 : nullptr;   // weights of A (from b)
     hipError_t e = hipSuccess;
-    if (style == BAKRON_SHAMPOO) {
-        wa = reinterpret_cast<float*>(static_cast<char*>(work) + align256(part));
-        wb = reinterpret_cast<float*>(reinterpret_cast<char*>(wa) + wbytes);
-        if ((e = bk::run_sample_weights(stream, a, N, n, nullptr, wa)) != hipSuccess ||
-            (e = bk::run_sample_weights(stream, b, N, m, nullptr, wb)) != hipSuccess)
-            return hess_hip(e, "bakron_kron_factors: weights");
+    for (int it = 1; it <= (shampoo ? iters : 1); ++it) {
+        if (shampoo && it == 1) {
+            if ((e = bk::run_sample_weights(stream, a, N, n, nullptr, wa)) != hipSuccess ||
+                (e = bk::run_sample_weights(stream, b, N, m, nullptr, wb)) != hipSuccess)
+                return hess_hip(e, who);
+        } else if (shampoo) {
+            if ((e = bk::run_quadform(stream, a, N, n, A, wa, h.part)) != hipSuccess ||
+                (e = bk::run_quadform(stream, b, N, m, B, wb, h.part)) != hipSuccess)
+                return hess_hip(e, who);
+        }
+        if ((e = bk::run_gram(stream, ga, a, N, n, wb, inv, nullptr, A, h.part)) != hipSuccess ||
+            (e = bk::run_gram(stream, gb, b, N, m, wa, inv, nullptr, B, h.part)) != hipSuccess)
+            return hess_hip(e, who);
     }
-    if ((e = bk::run_gram(stream, ga, a, N, n, wb, inv, nullptr, A, P)) != hipSuccess ||
-        (e = bk::run_gram(stream, gb, b, N, m, wa, inv, nullptr, B, P)) != hipSuccess)
-        return hess_hip(e, "bakron_kron_factors: gram");
     return BAKRON_OK;
+}
+
+// MLP-local case, App. A, b = D_g W_down^T: b b^T = (g g^T) (.) D^T D and
+// tr(b^T X b) = g^T (X (.) D^T D) g.  Step 1 of Shampoo weighs A by
+// g^T diag(D^T D) g and B by |x|^2; step i > 1 by g^T (B^(i-1) (.) D^T D) g
+// and x^T A^(i-1) x.
+static bakron_status mlp_local_impl(const char* who, const float* x, const float* g,
+                                    const float* D, int64_t N, int64_t dm, int64_t dff,
+                                    bool shampoo, int iters, float* A, float* B, void* work,
+                                    size_t* work_bytes, hipStream_t stream) {
+    if (N <= 0 || dm <= 0 || dff <= 0 || N > HESS_N_MAX || dm > HESS_DIM_MAX || dff > HESS_DIM_MAX ||
+        iters < 1 || iters > 64)
+        return hess_fail("bad size or iteration count");
+    if (iters > 1 && ((N + bk::GB - 1) / bk::GB) * ((std::max(dm, dff) + bk::GB - 1) / bk::GB) >
+                         ((int64_t)1 << 31) - 1)
+        return hess_fail("too many samples for the power steps");
+    const bool multi = shampoo && iters > 1;
+    const int ncu = bk::device_cus();
+    const GramGeom gx = bk::gram_geom(N, dm, ncu), gg = bk::gram_geom(N, dff, ncu),
+                   gd = bk::gram_geom(dm, dff, ncu);
+    size_t part = std::max({bk::gram_part_bytes(gx), bk::gram_part_bytes(gg),
+                            bk::gram_part_bytes(gd)});
+    if (multi)
+        part = std::max({part, bk::quadform_part_bytes(N, dm), bk::quadform_part_bytes(N, dff)});
+    const size_t wbytes = shampoo ? align256((size_t)N * sizeof(float)) : 0;
+    // extra: the diagonal of D^T D (step 1), and D^T D itself kept apart from B
+    // for the later steps
+    const size_t cbytes = shampoo ? align256((size_t)dff * sizeof(float)) : 0;
+    const size_t dbytes = multi ? (size_t)dff * (size_t)dff * sizeof(float) : 0;
+    bool query;
+    bakron_status st =
+        workspace_check(work, work_bytes, align256(part) + 2 * wbytes + cbytes + dbytes, &query);
+    if (st != BAKRON_OK || query) return st;
+    if (!x || !g || !D || !A || !B) return hess_fail("null pointer");
+    const HessWork h = carve(work, part, wbytes);
+    const float inv = (float)(1.0 / (double)N);
+    float* wx = shampoo ? h.w0 : nullptr;   // weights of B (from x)
+    float* wg = shampoo ? h.w1 : nullptr;   // weights of A (from g)
+    float* cdiag = h.extra;
+    float* DtD = multi ? reinterpret_cast<float*>(reinterpret_cast<char*>(h.extra) + cbytes) : B;
+    hipError_t e;
+    // D^T D (rows of D = W_down as samples)
+    if ((e = bk::run_gram(stream, gd, D, dm, dff, nullptr, 1.0f, nullptr, DtD, h.part)) != hipSuccess)
+        return hess_hip(e, who);
+    const int64_t nn = dff * dff;
+    for (int it = 1; it <= (shampoo ? iters : 1); ++it) {
+        if (shampoo && it == 1) {
+            hipLaunchKernelGGL(bk::k_diag, dim3((unsigned)((dff + 255) / 256)), dim3(256), 0, stream,
+                               DtD, dff, cdiag);
+            if ((e = hipGetLastError()) != hipSuccess ||
+                (e = bk::run_sample_weights(stream, g, N, dff, cdiag, wg)) != hipSuccess ||
+                (e = bk::run_sample_weights(stream, x, N, dm, nullptr, wx)) != hipSuccess)
+                return hess_hip(e, who);
+        } else if (shampoo) {
+            // B <- B^(i-1) (.) D^T D, the matrix of g's quadratic form
+            hipLaunchKernelGGL(bk::k_hadamard, dim3((unsigned)((nn + 255) / 256)), dim3(256), 0, stream,
+                               B, DtD, nn, B);
+            if ((e = hipGetLastError()) != hipSuccess ||
+                (e = bk::run_quadform(stream, g, N, dff, B, wg, h.part)) != hipSuccess ||
+                (e = bk::run_quadform(stream, x, N, dm, A, wx, h.part)) != hipSuccess)
+                return hess_hip(e, who);
+        }
+        // A = E[w_g x x^T]; B = E[w_x g g^T] (.) D^T D (in place over D^T D in
+        // the one-step case)
+        if ((e = bk::run_gram(stream, gx, x, N, dm, wg, inv, nullptr, A, h.part)) != hipSuccess ||
+            (e = bk::run_gram(stream, gg, g, N, dff, wx, inv, DtD, B, h.part)) != hipSuccess)
+            return hess_hip(e, who);
+    }
+    return BAKRON_OK;
+}
+
+extern "C" bakron_status bakron_kron_factors(const float* a, const float* b, int64_t N, int64_t n,
+                                             int64_t m, int32_t style, float* A, float* B,
+                                             void* work, size_t* work_bytes, hipStream_t stream) {
+    bk::set_last_error("");
+    if (style != BAKRON_KFAC && style != BAKRON_SHAMPOO) return hess_fail("bad style");
+    return kron_factors_impl("bakron_kron_factors", a, b, N, n, m, style == BAKRON_SHAMPOO, 1, A, B,
+                             work, work_bytes, stream);
+}
+
+extern "C" bakron_status bakron_kron_factors_iter(const float* a, const float* b, int64_t N,
+                                                  int64_t n, int64_t m, int32_t iters, float* A,
+                                                  float* B, void* work, size_t* work_bytes,
+                                                  hipStream_t stream) {
+    bk::set_last_error("");
+    return kron_factors_impl("bakron_kron_factors_iter", a, b, N, n, m, true, iters, A, B, work,
+                             work_bytes, stream);
 }
 
 extern "C" bakron_status bakron_mlp_local_factors(const float* x, const float* g, const float* D,
@@ -473,42 +754,36 @@ extern "C" bakron_status bakron_mlp_local_factors(const float* x, const float* g
                                                   float* A, float* B, void* work, size_t* work_bytes,
                                                   hipStream_t stream) {
     bk::set_last_error("");
-    if (N <= 0 || dm <= 0 || dff <= 0 || N > HESS_N_MAX || dm > HESS_DIM_MAX || dff > HESS_DIM_MAX)
-        return hess_fail("bad size");
     if (style != BAKRON_KFAC && style != BAKRON_SHAMPOO) return hess_fail("bad style");
-    const int ncu = bk::device_cus();
-    const GramGeom gx = bk::gram_geom(N, dm, ncu), gg = bk::gram_geom(N, dff, ncu),
-                   gd = bk::gram_geom(dm, dff, ncu);
-    const size_t part = std::max({bk::gram_part_bytes(gx), bk::gram_part_bytes(gg),
-                                  bk::gram_part_bytes(gd)});
-    const size_t wbytes = style == BAKRON_SHAMPOO ? align256((size_t)N * sizeof(float)) : 0;
-    const size_t cbytes = style == BAKRON_SHAMPOO ? align256((size_t)dff * sizeof(float)) : 0;
+    return mlp_local_impl("bakron_mlp_local_factors", x, g, D, N, dm, dff, style == BAKRON_SHAMPOO, 1,
+                          A, B, work, work_bytes, stream);
+}
+
+extern "C" bakron_status bakron_mlp_local_factors_iter(const float* x, const float* g,
+                                                       const float* D, int64_t N, int64_t dm,
+                                                       int64_t dff, int32_t iters, float* A,
+                                                       float* B, void* work, size_t* work_bytes,
+                                                       hipStream_t stream) {
+    bk::set_last_error("");
+    return mlp_local_impl("bakron_mlp_local_factors_iter", x, g, D, N, dm, dff, true, iters, A, B,
+                          work, work_bytes, stream);
+}
+
+extern "C" bakron_status bakron_quadform_weights(const float* X, int64_t N, int64_t d,
+                                                 const float* M, float* w, void* work,
+                                                 size_t* work_bytes, hipStream_t stream) {
+    bk::set_last_error("");
+    if (N < 0 || d < 0 || N > HESS_N_MAX || d > HESS_DIM_MAX ||
+        ((N + bk::GB - 1) / bk::GB) * ((d + bk::GB - 1) / bk::GB) > ((int64_t)1 << 31) - 1)
+        return hess_fail("bad size");
     bool query;
-    bakron_status st = workspace_check(work, work_bytes, align256(part) + 2 * wbytes + cbytes, &query);
+    bakron_status st = workspace_check(work, work_bytes, bk::quadform_part_bytes(N, d), &query);
     if (st != BAKRON_OK || query) return st;
-    if (!x || !g || !D || !A || !B) return hess_fail("null pointer");
-    float* P = static_cast<float*>(work);
-    const float inv = (float)(1.0 / (double)N);
-    hipError_t e;
-    // D^T D (rows of D = W_down as samples) into B
-    if ((e = bk::run_gram(stream, gd, D, dm, dff, nullptr, 1.0f, nullptr, B, P)) != hipSuccess)
-        return hess_hip(e, "bakron_mlp_local_factors: D^T D");
-    float* wx = nullptr;   // |x_k|^2, weights of B
-    float* wg = nullptr;   // g_k^T diag(D^T D) g_k = tr(b_k^T b_k), weights of A
-    if (style == BAKRON_SHAMPOO) {
-        wx = reinterpret_cast<float*>(static_cast<char*>(work) + align256(part));
-        wg = reinterpret_cast<float*>(reinterpret_cast<char*>(wx) + wbytes);
-        float* cdiag = reinterpret_cast<float*>(reinterpret_cast<char*>(wg) + wbytes);
-        hipLaunchKernelGGL(bk::k_diag, dim3((unsigned)((dff + 255) / 256)), dim3(256), 0, stream, B,
-                           dff, cdiag);
-        if ((e = hipGetLastError()) != hipSuccess ||
-            (e = bk::run_sample_weights(stream, g, N, dff, cdiag, wg)) != hipSuccess ||
-            (e = bk::run_sample_weights(stream, x, N, dm, nullptr, wx)) != hipSuccess)
-            return hess_hip(e, "bakron_mlp_local_factors: weights");
+    if (N > 0 && (!w || (d > 0 && (!X || !M)))) return hess_fail("null pointer");
+    if (d == 0) {   // empty forms: w = 0 (the weight kernel with no features)
+        hipError_t e = bk::run_sample_weights(stream, X, N, 0, nullptr, w);
+        return e == hipSuccess ? BAKRON_OK : hess_hip(e, "bakron_quadform_weights");
     }
-    // A = E[w_g x x^T]; B = E[w_x g g^T] (.) D^T D, in place over D^T D
-    if ((e = bk::run_gram(stream, gx, x, N, dm, wg, inv, nullptr, A, P)) != hipSuccess ||
-        (e = bk::run_gram(stream, gg, g, N, dff, wx, inv, B, B, P)) != hipSuccess)
-        return hess_hip(e, "bakron_mlp_local_factors: gram");
-    return BAKRON_OK;
+    hipError_t e = bk::run_quadform(stream, X, N, d, M, w, static_cast<float*>(work));
+    return e == hipSuccess ? BAKRON_OK : hess_hip(e, "bakron_quadform_weights: launch");
 }

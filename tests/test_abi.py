@@ -150,3 +150,32 @@ def test_binding_checks_quantiser_shapes():
         pk.mse_scales(torch.zeros(4, 4), 3)
     with pytest.raises((TypeError, ValueError)):
         pk._lib._quantizer(3, torch.zeros(4), 4, 8, "sym", 0, None)
+
+
+def test_power_step_host_validation(lib):
+    import paper_2608_06291_amd as pk
+    one = ctypes.c_void_p(256)
+    q = ctypes.c_size_t(0)
+    for iters in (0, 65):
+        assert lib.bakron_kron_factors_iter(one, one, 64, 32, 48, iters, one, one, None,
+                                            ctypes.byref(q), None) == pk.BAKRON_EINVAL
+        assert lib.bakron_mlp_local_factors_iter(one, one, one, 64, 32, 48, iters, one, one, None,
+                                                 ctypes.byref(q), None) == pk.BAKRON_EINVAL
+    # more steps need the quadratic-form partials (and D^T D for the MLP-local case)
+    assert lib.bakron_kron_factors_iter(one, one, 4096, 32, 48, 1, one, one, None,
+                                        ctypes.byref(q), None) == pk.BAKRON_OK
+    one_step = q.value
+    assert lib.bakron_mlp_local_factors_iter(one, one, one, 4096, 32, 48, 1, one, one, None,
+                                             ctypes.byref(q), None) == pk.BAKRON_OK
+    mlp1 = q.value
+    assert lib.bakron_mlp_local_factors_iter(one, one, one, 4096, 32, 48, 3, one, one, None,
+                                             ctypes.byref(q), None) == pk.BAKRON_OK
+    assert q.value >= mlp1 + 48 * 48 * 4
+    assert lib.bakron_kron_factors_iter(one, one, 4096, 32, 48, 3, one, one, None,
+                                        ctypes.byref(q), None) == pk.BAKRON_OK
+    assert q.value >= one_step
+    assert lib.bakron_quadform_weights(None, 10, 8, None, None, None, ctypes.byref(q),
+                                       None) == pk.BAKRON_OK and q.value >= 40
+    q2 = ctypes.c_size_t(q.value)
+    assert lib.bakron_quadform_weights(None, 10, 8, one, one, one, ctypes.byref(q2),
+                                       None) == pk.BAKRON_EINVAL

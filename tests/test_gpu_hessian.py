@@ -166,3 +166,89 @@ def test_mlp_local_factors_parity(oracle_mod, style, which, N, dm, dff):
     _check(A.cpu().numpy(), eA, _abssum(x, wA, 1.0 / N), N + dff, dm, f"mlp-A-{style}-{which}")
     _check(B.cpu().numpy(), eB, _abssum(g, wB, 1.0 / N, DtD_abs), N + dm, max(dm, dff),
            f"mlp-B-{style}-{which}")
+
+
+@pytest.mark.parametrize("N,d", [(1, 1), (300, 130), (1000, 258), (513, 256)])
+def test_quadform_weights_parity(oracle_mod, N, d):
+    """w_k = x_k^T M x_k against the oracle's per-sample trace tr(x^T M x):
+    a sum of d inner sums of d products each, so the fp32 bound is
+    (2d + 8) u |x|^T |M| |x| per sample."""
+    import torch
+    import paper_2608_06291_amd as pk
+    log(f"case quadform N={N} d={d}")
+    r = np.random.Generator(np.random.PCG64(np.random.SeedSequence([4100, N, d])))
+    X = workloads.ar1_samples(N, d, 0.4, r, norm_sigma=0.5)
+    Z = r.standard_normal((d, d + 3))
+    M = (Z @ Z.T / d).astype(np.float32)
+    w = pk.quadform_weights(_dev(X), _dev(M))
+    torch.cuda.synchronize()
+    w = w.cpu().numpy().astype(np.float64)
+    expect = oracle_mod.hessian.trace_quad(X, M.astype(np.float64))
+    Xa = np.abs(X.astype(np.float64))
+    bound = (2 * d + 8) * U32 * np.einsum("kj,jt,kt->k", Xa, np.abs(M.astype(np.float64)), Xa)
+    assert np.all(np.abs(w - expect) <= bound + 1e-30)
+
+
+def _iter_tol(N, d, iters):
+    """Relative Frobenius tolerance of `iters` power steps: each step adds a
+    Gram's and a quadratic form's fp32 error on top of the previous pair's."""
+    return iters * 40 * np.sqrt(N + 2 * d) * U32
+
+
+@pytest.mark.parametrize("iters", [2, 3])
+@pytest.mark.parametrize("N,n,m", [(2000, 200, 130), (257, 33, 70)])
+def test_kron_factors_power_steps(oracle_mod, iters, N, n, m):
+    import torch
+    import paper_2608_06291_amd as pk
+    h = oracle_mod.hessian
+    log(f"case shampoo iters={iters} N={N} n={n} m={m}")
+    p = workloads.kron_samples(N, n, m, seed=3)
+    A, B = pk.kron_factors(_dev(p["a"]), _dev(p["b"]), "shampoo", iters=iters)
+    torch.cuda.synchronize()
+    eA, eB = h.shampoo_factors(p["a"], p["b"], iters=iters)
+    for got, exp, d, lab in ((A, eA, n, "A"), (B, eB, m, "B")):
+        got = got.cpu().numpy().astype(np.float64)
+        rel = np.linalg.norm(got - exp) / np.linalg.norm(exp)
+        log(f"[shampoo{iters}] {lab} rel fro {rel:.2e}")
+        assert rel <= _iter_tol(N, d, iters), (lab, rel)
+        assert np.array_equal(got, got.T)
+
+
+@pytest.mark.parametrize("iters", [2, 3])
+def test_mlp_local_power_steps(oracle_mod, iters):
+    """The oracle forms b = D_g W_down^T and tr(b^T B b) explicitly; the GPU
+    uses g^T (B (.) D^T D) g."""
+    import torch
+    import paper_2608_06291_amd as pk
+    h = oracle_mod.hessian
+    N, dm, dff = 300, 64, 96
+    log(f"case mlp-local shampoo iters={iters}")
+    p = workloads.mlp_samples(N, dm, dff, seed=4)
+    A, B = pk.mlp_local_factors(_dev(p["x"]), _dev(p["g"]), _dev(p["Wd"]), "shampoo", iters=iters)
+    torch.cuda.synchronize()
+    eA, eB = h.mlp_local_factors(p["x"], p["g"], p["Wd"], "shampoo", iters=iters)
+    for got, exp, lab in ((A, eA, "A"), (B, eB, "B")):
+        got = got.cpu().numpy().astype(np.float64)
+        rel = np.linalg.norm(got - exp) / np.linalg.norm(exp)
+        log(f"[mlp shampoo{iters}] {lab} rel fro {rel:.2e}")
+        assert rel <= _iter_tol(N + dm, dff, iters), (lab, rel)
+
+
+def test_power_step_one_is_single_shampoo():
+    """iters = 1 through the iterating entry point is the one-step pair, bit
+    for bit."""
+    import torch
+    import paper_2608_06291_amd as pk
+    p = workloads.kron_samples(700, 100, 60, seed=5)
+    a, b = _dev(p["a"]), _dev(p["b"])
+    A1, B1 = pk.kron_factors(a, b, "shampoo")
+    lib = pk.load()
+    import ctypes
+    A2 = torch.empty_like(A1)
+    B2 = torch.empty_like(B1)
+    st = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    pk._lib._with_workspace(lambda wk, nb: lib.bakron_kron_factors_iter(
+        pk._lib._ptr(a), pk._lib._ptr(b), 700, 100, 60, 1, pk._lib._ptr(A2), pk._lib._ptr(B2), wk,
+        nb, st), a.device)
+    torch.cuda.synchronize()
+    assert torch.equal(A1, A2) and torch.equal(B1, B2)
