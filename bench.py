@@ -167,7 +167,8 @@ def table3(max_antidiag_elems: int):
 # projection with a backpropagated (global) Hessian.
 FACTOR_N = 256 * 2048
 FACTOR_WORKLOADS = (("mlp-local-up-4096x14336", "kfac"), ("mlp-local-up-4096x14336", "shampoo"),
-                    ("global-4096x4096", "kfac"), ("global-4096x4096", "shampoo"))
+                    ("global-4096x4096", "kfac"), ("global-4096x4096", "shampoo"),
+                    ("global-4096x4096", "shampoo3"))
 
 
 def _gram_flops(N: int, d: int) -> float:
@@ -211,13 +212,18 @@ def factors_bench(steps: int, warmup: int, n_samples: int, cpu_seconds: float, d
             torch.cuda.synchronize()
         a, b, D = cache[name]
         n, m = a.shape[1], b.shape[1]
+        iters = int(style[len("shampoo"):] or 1) if style.startswith("shampoo") else 1
+        base_style = "shampoo" if iters > 1 else style
         if D is not None:
-            run = lambda: pk.mlp_local_factors(a, b, D, style)  # noqa: E731
+            run = lambda: pk.mlp_local_factors(a, b, D, base_style, iters=iters)  # noqa: E731
             # D^T D over the dm rows of D, then the two N-sample Grams
             F = _gram_flops(D.shape[0], m) + _gram_flops(N, n) + _gram_flops(N, m)
         else:
-            run = lambda: pk.kron_factors(a, b, style)  # noqa: E731
+            run = lambda: pk.kron_factors(a, b, base_style, iters=iters)  # noqa: E731
             F = _gram_flops(N, n) + _gram_flops(N, m)
+        # each later power step adds the two Grams and the two quadratic forms
+        # (2 N d^2 flops for the product X M, N d for the fused row sums)
+        F = F * iters + (iters - 1) * (2.0 * N * (n * n + m * m) + N * (n + m))
         for _ in range(warmup):
             A, B = run()
         torch.cuda.synchronize()
@@ -229,7 +235,7 @@ def factors_bench(steps: int, warmup: int, n_samples: int, cpu_seconds: float, d
         ms = e0.elapsed_time(e1) / steps
         # the dominant launch pair: the Gram of the wider operand b over N samples
         # (k_gram and its slice reduction; the mask and weights as in the step)
-        w = pk.sample_weights(a) if style == "shampoo" else None
+        w = pk.sample_weights(a) if base_style == "shampoo" else None
         M = None
         if D is not None:
             M = pk.gram(D, None, 1.0)
@@ -245,7 +251,24 @@ def factors_bench(steps: int, warmup: int, n_samples: int, cpu_seconds: float, d
         torch.cuda.synchronize()
         g_ms = e0.elapsed_time(e1) / reps
         g_tf = _gram_flops(N, m) / (g_ms * 1e-3) / 1e12
-        # sampled parity: 48 entries of A and B against the fp64 oracle
+        q_ms = q_tf = None
+        if iters > 1:
+            # the power steps' quadratic form of the wider operand, timed alone
+            wq = torch.empty((N,), dtype=torch.float32, device=dev)
+            pk.quadform_weights(b, B, wq)
+            torch.cuda.synchronize()
+            e0.record(stream)
+            for _ in range(reps):
+                pk.quadform_weights(b, B, wq)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            q_ms = e0.elapsed_time(e1) / reps
+            q_tf = (2.0 * N * m * m + N * m) / (q_ms * 1e-3) / 1e12
+            del wq
+        # sampled parity: 48 entries of A and B against the fp64 oracle (one
+        # power step: the later steps' weights need the whole previous pair,
+        # which the oracle cannot form at this size; their parity is tested
+        # at smaller sizes)
         import oracle
         h = oracle.hessian
         rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([5000, n, m])))
@@ -270,27 +293,29 @@ def factors_bench(steps: int, warmup: int, n_samples: int, cpu_seconds: float, d
 
         pa, pb = pairs(n), pairs(m)
         wA = wB = None
-        if style == "shampoo":
+        rel = None
+        if base_style == "shampoo" and iters == 1:
             if D is not None:
                 Dn = D.double().cpu().numpy()
                 wA = wts(b, np.sum(Dn * Dn, axis=0))   # g^T diag(D^T D) g
             else:
                 wA = wts(b)
             wB = wts(a)
-        sa, qa = cols(a, pa)
-        sb, qb = cols(b, pb)
-        eA = h.expect_outer_entries(sa, qa, wA)
-        eB = h.expect_outer_entries(sb, qb, wB)
-        if D is not None:
-            sd, qd = cols(D, pb)
-            eB = eB * D.shape[0] * h.expect_outer_entries(sd, qd)
-        gA = np.array([A[i, j].item() for i, j in pa])
-        gB = np.array([B[i, j].item() for i, j in pb])
-        rel = float(max(np.max(np.abs(gA - eA) / np.abs(eA).max()),
-                        np.max(np.abs(gB - eB) / np.abs(eB).max())))
+        if iters == 1:
+            sa, qa = cols(a, pa)
+            sb, qb = cols(b, pb)
+            eA = h.expect_outer_entries(sa, qa, wA)
+            eB = h.expect_outer_entries(sb, qb, wB)
+            if D is not None:
+                sd, qd = cols(D, pb)
+                eB = eB * D.shape[0] * h.expect_outer_entries(sd, qd)
+            gA = np.array([A[i, j].item() for i, j in pa])
+            gB = np.array([B[i, j].item() for i, j in pb])
+            rel = float(max(np.max(np.abs(gA - eA) / np.abs(eA).max()),
+                            np.max(np.abs(gB - eB) / np.abs(eB).max())))
         cpu = None
         if do_cpu:
-            cpu = factors_cpu_baseline(a, b, D, style, F, cpu_seconds)
+            cpu = factors_cpu_baseline(a, b, D, base_style, iters, F, cpu_seconds)
         out = {
             "metric": "Kronecker-factor construction TFLOP/s (App. A), 1 MI355X",
             "value": F / (ms * 1e-3) / 1e12, "unit": "TFLOP/s", "n_gpus": 1, "steps": steps,
@@ -306,15 +331,20 @@ def factors_bench(steps: int, warmup: int, n_samples: int, cpu_seconds: float, d
                          "launch_ms": g_ms},
             "cpu_baseline": cpu,
         }
+        if q_ms is not None:
+            out["quadform"] = {"kernel": "k_quadform + k_quadform_reduce (N x %d operand)" % m,
+                               "bound": "mfma", "achieved": q_tf, "peak": PEAK_FP32_MFMA,
+                               "unit": "TFLOP/s", "frac": q_tf / PEAK_FP32_MFMA, "launch_ms": q_ms}
         print(json.dumps(out), flush=True)
         log(f"[factors] {name} {style}: {ms:.1f} ms/step, {out['value']:.1f} TFLOP/s; "
             f"Gram {g_ms:.1f} ms = {g_tf:.1f} TFLOP/s ({100 * g_tf / PEAK_FP32_MFMA:.0f}% of fp32 "
-            f"MFMA peak); sampled rel err {rel:.2e}")
+            f"MFMA peak)" + (f"; quadratic form {q_ms:.1f} ms = {q_tf:.1f} TFLOP/s" if q_ms else "")
+            + (f"; sampled rel err {rel:.2e}" if rel is not None else ""))
         del A, B, C, work, M, w
     cache.clear()
 
 
-def factors_cpu_baseline(a, b, D, style, F, seconds):
+def factors_cpu_baseline(a, b, D, style, iters, F, seconds):
     """Time the fp64 oracle on the first samples of the same workload
     (K-FAC / Shampoo factors from its per-sample definitions, the MLP-local b
     formed explicitly) and extrapolate linearly in the number of samples."""
@@ -327,11 +357,11 @@ def factors_cpu_baseline(a, b, D, style, F, seconds):
         sb = b[:k].double().cpu().numpy()
         t0 = time.perf_counter()
         if D is not None:
-            h.mlp_local_factors(sa, sb, D.double().cpu().numpy(), style)
+            h.mlp_local_factors(sa, sb, D.double().cpu().numpy(), style, iters=iters)
         elif style == "kfac":
             h.kfac_factors(sa, sb)
         else:
-            h.shampoo_factors(sa, sb, iters=1)
+            h.shampoo_factors(sa, sb, iters=iters)
         t = time.perf_counter() - t0
         if t >= seconds / 4 or k >= N:
             break

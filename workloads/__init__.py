@@ -226,6 +226,19 @@ def mlp_samples_torch(N: int, dm: int, dff: int, seed: int, device, feature: str
     return dict(x=x, Wg=Wg, Wu=Wu, Wd=Wd, feat=feat.contiguous())
 
 
+def toy_mlp(L: int, d: int, N: int, seed: int) -> dict:
+    """A stack of L square layers (y = W x, then SiLU) for the flow of Sec. 5:
+    W_l ~ N(0, 2/d), inputs x0 as in kron_samples (AR(1) rows with a spike and
+    log-normal norms), and output gradients g_out ~ N(0, 1) standing in for
+    the gradients of sampled-label losses (App. D), all fp32."""
+    r = [np.random.Generator(np.random.PCG64(np.random.SeedSequence([4000, L, d, N, seed, k])))
+         for k in range(3)]
+    W = [(r[0].standard_normal((d, d)) * np.sqrt(2.0 / d)).astype(np.float32) for _ in range(L)]
+    x0 = ar1_samples(N, d, 0.5, r[1], spike_rank=min(4, d), spike_rng=r[2], norm_sigma=0.5)
+    g_out = r[2].standard_normal((N, d)).astype(np.float32)
+    return dict(W=W, x0=x0, g_out=g_out)
+
+
 def make_weights(cfg: Config, seed: int) -> np.ndarray:
     rng = _rng(cfg.cid, seed, STREAM_W)
     if cfg.heavy_tail:
