@@ -378,6 +378,136 @@ def factors_cpu_baseline(a, b, D, style, iters, F, seconds):
                 s_per_step=t_full, host_cpu=cpu_model())
 
 
+def quant_bench(steps: int):
+    """Quantiser variants on the 4096 x 4096 layer (INT4): the solve with
+    per-row symmetric scales against the general path (asymmetric alphabet,
+    128-column group scales, per-column factors), and the MSE scale search
+    (App. D) per row and per 128-column group.  One JSON line each."""
+    import numpy as np
+    import torch
+    import paper_2608_06291_amd as pk
+    import workloads
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.Stream(dev)
+    torch.cuda.set_stream(stream)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+
+    def timed(fn, reps):
+        fn()
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(reps):
+            fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps
+
+    c = workloads.make(2, seed=0, device="cuda")
+    m, n = c["cfg"].m, c["cfg"].n
+    W = torch.from_numpy(c["W"]).to(dev)
+    f = pk.factor(torch.from_numpy(c["A"]).to(dev), torch.from_numpy(c["B"]).to(dev), c["damp"])
+    codes = torch.empty((m, n), dtype=torch.int8, device=dev)
+    V = torch.empty((m, n), dtype=torch.float32, device=dev)
+    s_row = torch.from_numpy(c["scale"]).to(dev)
+    s_grp = pk.mse_scales(W, 4, "asym", group_size=128)
+    col = torch.from_numpy(np.random.Generator(np.random.PCG64(5)).uniform(0.75, 1.25, n)
+                           .astype(np.float32)).to(dev)
+    F = float(m) * n * (m + n)
+    rows = []
+    for label, kw, sc in (("per-row symmetric", {}, s_row),
+                          ("asymmetric, 128-column groups, column factors",
+                           dict(alphabet="asym", group_size=128, col_scale=col), s_grp)):
+        ms = timed(lambda: pk.solve(W, f, 4, sc, codes=codes, V=V, **kw), steps)
+        rows.append(dict(kind="solve", quantiser=label, ms=ms, tflops=F / ms / 1e9))
+    for g in (0, 128):
+        ms = timed(lambda: pk.mse_scales(W, 4, "sym", group_size=g), steps)
+        # candidates x entries evaluated (one division, rint, product, fp64 square-add each)
+        rows.append(dict(kind="mse_scales", group_size=g, ms=ms,
+                         evaluations_per_s=101.0 * m * n / (ms * 1e-3)))
+    f.close()
+    for r in rows:
+        r.update(workload="attn-proj-4096x4096", bits=4)
+        print(json.dumps(r), flush=True)
+        log(f"[quant] {r}")
+
+
+def flow_bench(L: int, d: int, N: int, style: str):
+    """Sec. 5's recursive flow over a stack of L square layers (width d, N
+    calibration samples, SiLU): per phase, the summed device time of the
+    model's forward/backward, the Kronecker factors, the factorisation, the
+    scale search and the BaKron solve, plus the layer-evaluation counts.  One
+    JSON line."""
+    import time as _t
+    import torch
+    import paper_2608_06291_amd as pk
+    from paper_2608_06291_amd import flow
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.Stream(dev)
+    torch.cuda.set_stream(stream)
+    gen = torch.Generator(device=dev).manual_seed(11)
+    W = [(torch.randn((d, d), generator=gen, device=dev) * (2.0 / d) ** 0.5) for _ in range(L)]
+    import workloads
+    x0 = workloads.ar1_samples_torch(N, d, 0.5, gen, dev, spike_rank=4, norm_sigma=0.5)
+    g_out = torch.randn((N, d), generator=gen, device=dev)
+    torch.cuda.synchronize()
+    phase = {k: 0.0 for k in ("model", "factors", "factorise", "scales", "solve")}
+
+    class Timed(flow.LayerStack):
+        def forward_layer(self, l, x, stats):
+            t0 = _tick()
+            out = super().forward_layer(l, x, stats)
+            phase["model"] += _tock(t0)
+            return out
+
+        def backward_layer(self, l, y, g, stats):
+            t0 = _tick()
+            out = super().backward_layer(l, y, g, stats)
+            phase["model"] += _tock(t0)
+            return out
+
+    def _tick():
+        e = torch.cuda.Event(enable_timing=True)
+        e.record(stream)
+        return e
+
+    def _tock(e):
+        e2 = torch.cuda.Event(enable_timing=True)
+        e2.record(stream)
+        e2.synchronize()
+        return e.elapsed_time(e2)
+
+    stack = Timed(W)
+    iters = int(style[len("shampoo"):] or 1) if style.startswith("shampoo") else 1
+    base = "shampoo" if style.startswith("shampoo") else "kfac"
+
+    def step(l, a, b):
+        t0 = _tick()
+        A, B = pk.kron_factors(a, b, base, iters=iters)
+        phase["factors"] += _tock(t0)
+        t0 = _tick()
+        f = pk.factor(A, B, 0.5)
+        phase["factorise"] += _tock(t0)
+        t0 = _tick()
+        sc = pk.mse_scales(stack.W[l], 3)
+        phase["scales"] += _tock(t0)
+        t0 = _tick()
+        pk.solve(stack.W[l], f, 3, sc)
+        phase["solve"] += _tock(t0)
+        f.close()
+
+    t0 = _t.perf_counter()
+    st = flow.recursive_flow(stack, x0, g_out, step)
+    torch.cuda.synchronize()
+    wall = _t.perf_counter() - t0
+    total = sum(phase.values())
+    out = dict(kind="flow", layers=L, width=d, samples=N, factors=style, wall_s=wall,
+               phase_ms=phase, core_share=phase["solve"] / total,
+               layer_forwards=st.layer_forwards, layer_backwards=st.layer_backwards,
+               peak_live_pairs=st.peak_live_pairs)
+    print(json.dumps(out), flush=True)
+    log(f"[flow] {out}")
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -399,6 +529,12 @@ def main():
     ap.add_argument("--factors", action="store_true",
                     help="only run the Kronecker-factor construction workloads (App. A: K-FAC and "
                          "single-step Shampoo, global and MLP-local) and exit; one JSON line each")
+    ap.add_argument("--quant", action="store_true",
+                    help="only time the quantiser variants and the MSE scale search on the "
+                         "4096 x 4096 layer and exit")
+    ap.add_argument("--flow", default=None, metavar="L,d,N[,style]",
+                    help="only run the recursive backprop flow (Sec. 5) over L layers of width d "
+                         "with N samples (style kfac or shampooK) and exit")
     ap.add_argument("--factor-only", default=None,
                     help="with --factors: run only this workload:style (e.g. global-4096x4096:kfac)")
     ap.add_argument("--factor-samples", type=int, default=FACTOR_N,
@@ -415,6 +551,15 @@ def main():
 
     if args.table3:
         table3(args.table3_max_antidiag_elems)
+        return
+
+    if args.quant:
+        quant_bench(args.steps)
+        return
+
+    if args.flow:
+        parts = args.flow.split(",")
+        flow_bench(int(parts[0]), int(parts[1]), int(parts[2]), parts[3] if len(parts) > 3 else "kfac")
         return
 
     if args.factors:

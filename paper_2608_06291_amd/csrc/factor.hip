@@ -11,7 +11,7 @@
 // Hence R^-1 = P C^-T P and L[i][j] = Cinv[n-1-j][n-1-i] * C[n-1-j][n-1-j].
 //
 // Blocked right-looking Cholesky (block NB) and a recursive triangular
-// inverse, both driven by one fp64 tiled GEMM.  The result is rounded once to
+// inverse, both driven by one fp64 GEMM on the matrix cores.  The result is rounded once to
 // fp32 and stored as packed lower-triangular TS x TS tiles for the solver.
 #include "common.h"
 
@@ -48,47 +48,80 @@ __global__ void k_flip_damp(const float* __restrict__ X, int64_t d, const double
 }
 
 // Unblocked Cholesky of the diagonal block Z[k0:k0+b, k0:k0+b] (lower part
-// only), one workgroup.  A non-positive or non-finite pivot sets *fail and
-// records the pivot index in the reversed ordering.
-__global__ __launch_bounds__(256) void k_potrf_diag(double* __restrict__ Z, int64_t ld, int64_t k0,
-                                                    int b, int* __restrict__ fail,
-                                                    int64_t* __restrict__ fail_pivot) {
+// only), one wave: lane i holds row i of the block in registers; column j is
+// finished by lane j's pivot (read by every lane through LDS), scaled in each
+// lane, published to LDS and used by every later row for its trailing
+// update.  LDS operations of one wave complete in order, so no barrier is
+// needed.  A non-positive or non-finite pivot sets *fail and records the
+// pivot index in the reversed ordering.
+__global__ __launch_bounds__(NB) void k_potrf_diag(double* __restrict__ Z, int64_t ld, int64_t k0,
+                                                   int b, int* __restrict__ fail,
+                                                   int64_t* __restrict__ fail_pivot) {
     if (*fail) return;
-    __shared__ double S[NB][NB + 1];
-    __shared__ double piv_s;
-    const int t = threadIdx.x;
-    for (int e = t; e < b * b; e += blockDim.x) {
-        const int i = e / b, j = e % b;
-        S[i][j] = (j <= i) ? Z[(k0 + i) * ld + (k0 + j)] : 0.0;
-    }
-    __syncthreads();
-    for (int j = 0; j < b; ++j) {
-        if (t == 0) piv_s = S[j][j];
-        __syncthreads();
-        const double piv = piv_s;
-        if (!(piv > 0.0) || !isfinite(piv)) {
-            if (t == 0) {
+    __shared__ double col[NB];
+    const int i = threadIdx.x;
+    double row[NB];
+#pragma unroll
+    for (int c = 0; c < NB; ++c) row[c] = (i < b && c <= i && c < b) ? Z[(k0 + i) * ld + (k0 + c)] : 0.0;
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+        if (j >= b) continue;                                // uniform (last, partial block)
+        if (i == j) col[j] = row[j];
+        __builtin_amdgcn_wave_barrier();
+        const double piv = col[j];
+        if (!(piv > 0.0) || !isfinite(piv)) {                 // uniform: one value for all lanes
+            if (i == 0) {
                 *fail = 1;
                 *fail_pivot = k0 + j;
             }
-            return;  // uniform: every thread read the same pivot
+            return;
         }
         const double dj = sqrt(piv);
-        __syncthreads();
-        for (int i = j + 1 + t; i < b; i += blockDim.x) S[i][j] /= dj;
-        if (t == 0) S[j][j] = dj;
-        __syncthreads();
-        const int r = b - j - 1;  // trailing order
-        for (int e = t; e < r * r; e += blockDim.x) {
-            const int i = j + 1 + e / r, c = j + 1 + e % r;
-            if (c <= i) S[i][c] -= S[i][j] * S[c][j];
-        }
-        __syncthreads();
+        if (i == j) row[j] = dj;
+        else if (i > j) row[j] /= dj;
+        __builtin_amdgcn_wave_barrier();
+        col[i] = row[j];                                     // column j of the factor (rows > j)
+        __builtin_amdgcn_wave_barrier();
+#pragma unroll
+        for (int c = j + 1; c < NB; ++c)
+            if (c <= i) row[c] = fma(-row[j], col[c], row[c]);
+        __builtin_amdgcn_wave_barrier();
     }
-    for (int e = t; e < b * b; e += blockDim.x) {
-        const int i = e / b, j = e % b;
-        if (j <= i) Z[(k0 + i) * ld + (k0 + j)] = S[i][j];
+    if (i < b) {
+#pragma unroll
+        for (int c = 0; c < NB; ++c)
+            if (c <= i && c < b) Z[(k0 + i) * ld + (k0 + c)] = row[c];
     }
+}
+
+// Panel of the blocked Cholesky: every row r >= k0 + b of Z[:, k0:k0+b] is
+// replaced by the solution x of x C_kk^T = Z[r, k0:k0+b] (C_kk the factored
+// diagonal block, lower): x_j = (p_j - sum_{c<j} x_c C_jc) / C_jj, one thread
+// per row, C_kk in LDS (read as broadcasts), x in registers.
+__global__ __launch_bounds__(256) void k_trsm_panel(double* __restrict__ Z, int64_t ld, int64_t k0,
+                                                    int b, int64_t rows,
+                                                    const int* __restrict__ fail) {
+    if (*fail) return;
+    __shared__ double Ck[NB][NB + 1];
+    for (int e = threadIdx.x; e < NB * NB; e += 256) {
+        const int i = e / NB, c = e % NB;
+        Ck[i][c] = (i < b && c <= i) ? Z[(k0 + i) * ld + (k0 + c)] : 0.0;
+    }
+    __syncthreads();
+    const int64_t r = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (r >= rows) return;
+    double* p = Z + (k0 + b + r) * ld + k0;
+    double x[NB];
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+        double v = j < b ? p[j] : 0.0;
+#pragma unroll
+        for (int c = 0; c < j; ++c) v = fma(-x[c], Ck[j][c], v);
+        x[j] = j < b ? v / Ck[j][j] : 0.0;
+    }
+#pragma unroll
+    for (int j = 0; j < NB; ++j)
+        if (j < b) p[j] = x[j];
 }
 
 // Inverse of lower-triangular diagonal blocks of C (size nbk <= NB each):
@@ -126,10 +159,17 @@ __global__ __launch_bounds__(NB) void k_inv_lower_blocks(const double* __restric
     }
 }
 
-// C[M x N] = alpha * A[M x K] * op(B) + beta * C, row-major fp64.
+// C[M x N] = alpha * A[M x K] * op(B) + beta * C, row-major fp64, on fp64
+// MFMA (v_mfma_f64_16x16x4f64: lane l supplies A[l % 16][l / 16] and
+// B[l / 16][l % 16] of a k-step; register r of lane l holds
+// D[l / 16 + 4 r][l % 16]).
 // op(B) = B (K x N, ldb) or B^T (B is N x K, ldb).  lower_only skips output
 // blocks lying entirely above the diagonal (row index < col index) of C.
-constexpr int GB = 64, GK = 16;
+// One workgroup per 64 x 64 block of C, 4 waves of 2 x 2 MFMA blocks; K in
+// chunks of 16 staged through double-buffered LDS as [k][row] / [k][col],
+// the next chunk loaded into registers while the current one is multiplied.
+typedef double f64x4 __attribute__((ext_vector_type(4)));
+constexpr int GB = 64, GK = 16, GPAD = GB + 2;
 __global__ __launch_bounds__(256) void k_gemm64(int64_t M, int64_t N, int64_t K, double alpha,
                                                 const double* __restrict__ A, int64_t lda,
                                                 const double* __restrict__ B, int64_t ldb,
@@ -139,63 +179,94 @@ __global__ __launch_bounds__(256) void k_gemm64(int64_t M, int64_t N, int64_t K,
     if (*fail) return;
     const int64_t r0 = (int64_t)blockIdx.y * GB, c0 = (int64_t)blockIdx.x * GB;
     if (lower_only && c0 > r0 + GB - 1) return;
-    __shared__ double As[GK][GB + 1];
-    __shared__ double Bs[GK][GB + 1];
+    __shared__ double As[2][GK][GPAD];
+    __shared__ double Bs[2][GK][GPAD];
     const int t = threadIdx.x;
-    const int tr = t / 16, tc = t % 16;
-    double acc[4][4];
+    const int wv = t >> 6, l = t & 63;
+    const int wm = wv >> 1, wn = wv & 1;
+    const int li = l & 15, lk = l >> 4;
+    // staging: A rows (and B^T rows) by t >> 2, k quarter 4 (t & 3); B rows
+    // (k) by t >> 4, column quarter 4 (t & 15)
+    const int ar = t >> 2, aq = 4 * (t & 3);
+    const int bk = t >> 4, bq = 4 * (t & 15);
+    double ra[4], rb[4];
+    auto load = [&](int64_t k0) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = 0.0;
-    for (int64_t k0 = 0; k0 < K; k0 += GK) {
-        // A tile: GB rows x GK cols -> As[k][r]
-        for (int e = t; e < GB * GK; e += 256) {
-            const int r = e / GK, k = e % GK;
-            const int64_t gr = r0 + r, gk = k0 + k;
-            As[k][r] = (gr < M && gk < K) ? A[gr * lda + gk] : 0.0;
+        for (int u = 0; u < 4; ++u) {
+            const int64_t gr = r0 + ar, gk = k0 + aq + u;
+            ra[u] = (gr < M && gk < K) ? A[gr * lda + gk] : 0.0;
         }
-        // op(B) tile: GK rows x GB cols -> Bs[k][c]
         if (!transB) {
-            for (int e = t; e < GB * GK; e += 256) {
-                const int k = e / GB, c = e % GB;
-                const int64_t gk = k0 + k, gc = c0 + c;
-                Bs[k][c] = (gk < K && gc < N) ? B[gk * ldb + gc] : 0.0;
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int64_t gk = k0 + bk, gc = c0 + bq + u;
+                rb[u] = (gk < K && gc < N) ? B[gk * ldb + gc] : 0.0;
             }
         } else {
-            for (int e = t; e < GB * GK; e += 256) {
-                const int c = e / GK, k = e % GK;
-                const int64_t gk = k0 + k, gc = c0 + c;
-                Bs[k][c] = (gk < K && gc < N) ? B[gc * ldb + gk] : 0.0;
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int64_t gc = c0 + ar, gk = k0 + aq + u;
+                rb[u] = (gk < K && gc < N) ? B[gc * ldb + gk] : 0.0;
             }
         }
-        __syncthreads();
+    };
+    auto store = [&](int sb) {
 #pragma unroll
-        for (int k = 0; k < GK; ++k) {
-            double a[4], bb[4];
+        for (int u = 0; u < 4; ++u) As[sb][aq + u][ar] = ra[u];
+        if (!transB) {
 #pragma unroll
-            for (int i = 0; i < 4; ++i) a[i] = As[k][tr * 4 + i];
+            for (int u = 0; u < 4; ++u) Bs[sb][bk][bq + u] = rb[u];
+        } else {
 #pragma unroll
-            for (int j = 0; j < 4; ++j) bb[j] = Bs[k][tc * 4 + j];
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-#pragma unroll
-                for (int j = 0; j < 4; ++j) acc[i][j] = fma(a[i], bb[j], acc[i][j]);
+            for (int u = 0; u < 4; ++u) Bs[sb][aq + u][ar] = rb[u];
         }
+    };
+    f64x4 acc[2][2];
+#pragma unroll
+    for (int x = 0; x < 2; ++x)
+#pragma unroll
+        for (int y = 0; y < 2; ++y) acc[x][y] = f64x4{0.0, 0.0, 0.0, 0.0};
+    const int64_t nch = (K + GK - 1) / GK;
+    if (nch > 0) {
+        load(0);
+        store(0);
+    }
+    __syncthreads();
+    for (int64_t c = 0; c < nch; ++c) {
+        const int sb = (int)(c & 1);
+        const bool more = c + 1 < nch;
+        if (more) load((c + 1) * GK);
+#pragma unroll
+        for (int kk = 0; kk < GK / 4; ++kk) {
+            const int kr = 4 * kk + lk;
+            double a[2], b2[2];
+#pragma unroll
+            for (int x = 0; x < 2; ++x) a[x] = As[sb][kr][wm * 32 + x * 16 + li];
+#pragma unroll
+            for (int y = 0; y < 2; ++y) b2[y] = Bs[sb][kr][wn * 32 + y * 16 + li];
+#pragma unroll
+            for (int x = 0; x < 2; ++x)
+#pragma unroll
+                for (int y = 0; y < 2; ++y)
+                    acc[x][y] = __builtin_amdgcn_mfma_f64_16x16x4f64(a[x], b2[y], acc[x][y], 0, 0, 0);
+        }
+        if (more) store(sb ^ 1);
         __syncthreads();
     }
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const int64_t gr = r0 + tr * 4 + i;
-        if (gr >= M) continue;
+    for (int x = 0; x < 2; ++x)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const int64_t gc = c0 + tc * 4 + j;
+        for (int y = 0; y < 2; ++y) {
+            const int64_t gc = c0 + wn * 32 + y * 16 + li;
             if (gc >= N) continue;
-            double* cp = C + gr * ldc + gc;
-            *cp = (beta == 0.0) ? alpha * acc[i][j] : alpha * acc[i][j] + beta * (*cp);
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int64_t gr = r0 + wm * 32 + x * 16 + lk + 4 * r;
+                if (gr >= M) continue;
+                double* cp = C + gr * ldc + gc;
+                *cp = (beta == 0.0) ? alpha * acc[x][y][r] : alpha * acc[x][y][r] + beta * (*cp);
+            }
         }
-    }
 }
 
 __global__ void k_copy2d(const double* __restrict__ src, int64_t lds, double* __restrict__ dst,
@@ -317,20 +388,12 @@ hipError_t factor_one(hipStream_t s, const float* X, int64_t d, double lam, doub
     if (e != hipSuccess) return e;
     for (int64_t k0 = 0; k0 < d; k0 += NB) {
         const int b = (int)((d - k0) < NB ? (d - k0) : NB);
-        hipLaunchKernelGGL(k_potrf_diag, dim3(1), dim3(256), 0, s, Z, d, k0, b, fail, fail_pivot);
+        hipLaunchKernelGGL(k_potrf_diag, dim3(1), dim3(NB), 0, s, Z, d, k0, b, fail, fail_pivot);
         const int64_t rest = d - k0 - b;
         if (rest > 0) {
-            // panel solve: P <- P * C_kk^-T via the explicit inverse of C_kk
-            double* Cinv = T;                 // NB x NB at the front of T
-            double* Ptmp = T + NB * NB;       // rest x b
-            hipMemsetAsync(Cinv, 0, sizeof(double) * NB * NB, s);
-            hipLaunchKernelGGL(k_inv_lower_blocks, dim3(1), dim3(NB), 0, s, Z, d, Cinv, (int64_t)NB,
-                               k0, k0 + b, (int64_t)0, fail);
-            e = gemm64(s, rest, b, b, 1.0, Z + (k0 + b) * d + k0, d, Cinv, NB, 1, 0.0, Ptmp, b, 0,
-                       fail);
-            if (e != hipSuccess) return e;
-            hipLaunchKernelGGL(k_copy2d, dim3(grid1d(rest * b)), dim3(256), 0, s, Ptmp, (int64_t)b,
-                               Z + (k0 + b) * d + k0, d, rest, (int64_t)b, fail);
+            // panel solve: P <- P C_kk^-T by substitution
+            hipLaunchKernelGGL(k_trsm_panel, dim3((unsigned)((rest + 255) / 256)), dim3(256), 0, s, Z,
+                               d, k0, b, rest, fail);
             // trailing update Z22 -= P P^T (lower blocks)
             e = gemm64(s, rest, rest, b, -1.0, Z + (k0 + b) * d + k0, d, Z + (k0 + b) * d + k0, d, 1,
                        1.0, Z + (k0 + b) * d + (k0 + b), d, 1, fail);
