@@ -159,8 +159,9 @@ constexpr int PULL_T0 = 2;        // first loop turn whose idle waves may consum
 // both of its entries.  Coefficients are register-resident, each factor row
 // rotated so that step d reads register (d mod 32).
 // GQ: scales per column group and/or per column (else one scale per row, the
-// same for both entries of a thread).
-template <bool GQ>
+// same for both entries of a thread).  ASYM: alphabet {qlo..qhi} (else the
+// symmetric {-qhi..qhi}, clamped with one scalar operand).
+template <bool GQ, bool ASYM>
 __global__ __launch_bounds__(512) void k_seg(SegArgs a) {
     __shared__ float LBt[TS][TS];            // unpadded: the rotated reads below are conflict-free
     __shared__ float LAt[TS][TS];
@@ -182,7 +183,7 @@ __global__ __launch_bounds__(512) void k_seg(SegArgs a) {
     const int c0 = 4 * w + 2 * hf;
     const int q0 = (c0 - p) & 31;
     const int q1 = (q0 + 1) & 31;
-    const float qlo = a.q.qlo, qhi = a.q.qhi;
+    const float qhi = a.q.qhi, qlo = ASYM ? a.q.qlo : -qhi;
     const int knear = a.knear;
     const bool roww = w < 4;   // wave-uniform: row-kind or column-kind pull blocks
 
@@ -229,7 +230,7 @@ __global__ __launch_bounds__(512) void k_seg(SegArgs a) {
             pf_g1 = a.Y[tb + p * TS + q1];
             const int row = I_first * TS + p;
             pf_s0 = row_scale_of<GQ>(a.q, row, cs0, a.m);
-            pf_s1 = GQ ? row_scale_of<GQ>(a.q, row, cs1, a.m) : pf_s0;
+            pf_s1 = GQ ? row_scale_of<GQ>(a.q, row, cs1, a.m) : 0.0f;
         }
 
         // pull state of the next tile (uniform): which operands are staged,
@@ -266,9 +267,10 @@ __global__ __launch_bounds__(512) void k_seg(SegArgs a) {
             float h0 = pf_h0, h1 = pf_h1;
             float g0 = pf_g0, g1 = pf_g1;
             const int row = I * TS + p;
-            const float s0 = pf_s0, s1 = pf_s1;   // scales of the thread's two entries
+            // scales of the thread's two entries (one per row without GQ)
+            const float s0 = pf_s0, s1 = GQ ? pf_s1 : s0;
             const float inv_s0 = (s0 > 0.0f) ? 1.0f / s0 : 0.0f;
-            const float inv_s1 = (s1 > 0.0f) ? 1.0f / s1 : 0.0f;
+            const float inv_s1 = GQ ? ((s1 > 0.0f) ? 1.0f / s1 : 0.0f) : inv_s0;
             const int kc = a.b_ident ? 0 : (knear < I ? knear : I);   // column sources k = 1..kc
 
             // multiplies source distance k of tile It into pacc (row or column kind)
@@ -369,7 +371,7 @@ __global__ __launch_bounds__(512) void k_seg(SegArgs a) {
                 pf_g1 = a.Y[tb + p * TS + q1];
                 const int rn = In * TS + p;
                 pf_s0 = row_scale_of<GQ>(a.q, rn, cs0, a.m);
-                pf_s1 = GQ ? row_scale_of<GQ>(a.q, rn, cs1, a.m) : pf_s0;
+                if (GQ) pf_s1 = row_scale_of<GQ>(a.q, rn, cs1, a.m);
             }
 
             float lbr[TS], lar0[TS], lar1[TS];
@@ -753,10 +755,15 @@ hipError_t run_plan(hipStream_t st, hipStream_t side, const Plan& plan, const fl
                 sa.nstrips = op.nstrips;
                 sa.counter = ws.counters + op.counter;
                 const int grid = op.nstrips < SEG_GRID ? op.nstrips : SEG_GRID;
-                if (q.gsize > 0 || q.col_scale)
-                    hipLaunchKernelGGL(k_seg<true>, dim3((unsigned)grid), dim3(512), 0, st, sa);
+                const bool gq = q.gsize > 0 || q.col_scale, asym = q.qlo != -q.qhi;
+                if (gq && asym)
+                    hipLaunchKernelGGL((k_seg<true, true>), dim3((unsigned)grid), dim3(512), 0, st, sa);
+                else if (gq)
+                    hipLaunchKernelGGL((k_seg<true, false>), dim3((unsigned)grid), dim3(512), 0, st, sa);
+                else if (asym)
+                    hipLaunchKernelGGL((k_seg<false, true>), dim3((unsigned)grid), dim3(512), 0, st, sa);
                 else
-                    hipLaunchKernelGGL(k_seg<false>, dim3((unsigned)grid), dim3(512), 0, st, sa);
+                    hipLaunchKernelGGL((k_seg<false, false>), dim3((unsigned)grid), dim3(512), 0, st, sa);
             } else {
                 node(op, st);
             }
