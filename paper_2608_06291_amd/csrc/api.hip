@@ -311,47 +311,71 @@ extern "C" bakron_status bakron_factor(const float* A, int64_t n, const float* B
         if (v >= 0 && v <= bk::KNEAR_MAX) f->knear = v;
     }
 
-    const int64_t dmax = (B && m > n) ? m : n;
+    // A and B are factored concurrently (their block steps are latency-bound):
+    // B on a second, non-blocking stream forked from and joined back into
+    // `stream`, each with its own scratch
     const int64_t ntA = cdiv(n, bk::TS);
-    double *Z = nullptr, *Ninv = nullptr, *T = nullptr, *scal = nullptr;
+    double *Z[2] = {nullptr, nullptr}, *Ninv[2] = {nullptr, nullptr}, *T[2] = {nullptr, nullptr};
+    double* scal = nullptr;
     int* flags = nullptr;
+    hipStream_t sB = nullptr;
+    hipEvent_t ev[2] = {nullptr, nullptr};
     bakron_status st = BAKRON_OK;
-    hipError_t e;
+    hipError_t e = hipSuccess;
     auto cleanup = [&]() {
-        if (Z) hipFree(Z);
-        if (Ninv) hipFree(Ninv);
-        if (T) hipFree(T);
+        for (int k = 0; k < 2; ++k) {
+            if (Z[k]) hipFree(Z[k]);
+            if (Ninv[k]) hipFree(Ninv[k]);
+            if (T[k]) hipFree(T[k]);
+            if (ev[k]) hipEventDestroy(ev[k]);
+        }
         if (scal) hipFree(scal);
         if (flags) hipFree(flags);
+        if (sB) hipStreamDestroy(sB);
     };
-    const size_t zbytes = sizeof(double) * (size_t)dmax * (size_t)dmax;
-    const size_t tbytes = sizeof(double) * ((size_t)dmax * (size_t)dmax / 4 + (size_t)dmax * 64 +
-                                            64 * 64 + 64);
-    if ((e = hipMalloc(&Z, zbytes)) != hipSuccess || (e = hipMalloc(&Ninv, zbytes)) != hipSuccess ||
-        (e = hipMalloc(&T, tbytes)) != hipSuccess ||
-        (e = hipMalloc(&scal, 4 * sizeof(double))) != hipSuccess ||
-        (e = hipMalloc(&flags, 8 * sizeof(int64_t))) != hipSuccess) {
+    for (int k = 0; k < (B ? 2 : 1) && e == hipSuccess; ++k) {
+        const size_t d = (size_t)(k == 0 ? n : m);
+        const size_t zbytes = sizeof(double) * d * d;
+        const size_t tbytes = sizeof(double) * (d * d / 4 + d * 64 + 64 * 64 + 64);
+        if ((e = hipMalloc(&Z[k], zbytes)) == hipSuccess && (e = hipMalloc(&Ninv[k], zbytes)) == hipSuccess)
+            e = hipMalloc(&T[k], tbytes);
+    }
+    if (e == hipSuccess) e = hipMalloc(&scal, 4 * sizeof(double));
+    if (e == hipSuccess) e = hipMalloc(&flags, 8 * sizeof(int64_t));
+    if (e != hipSuccess) {
         st = hip_fail(&g_last_error, e, "bakron_factor: hipMalloc (factor scratch)");
         cleanup();
         delete f;
         return st;
     }
     e = hipMemsetAsync(flags, 0, 8 * sizeof(int64_t), stream);
+    if (e == hipSuccess && B) {
+        e = hipStreamCreateWithFlags(&sB, hipStreamNonBlocking);
+        if (e == hipSuccess) e = hipEventCreateWithFlags(&ev[0], hipEventDisableTiming);
+        if (e == hipSuccess) e = hipEventCreateWithFlags(&ev[1], hipEventDisableTiming);
+        if (e == hipSuccess) e = hipEventRecord(ev[0], stream);
+        if (e == hipSuccess) e = hipStreamWaitEvent(sB, ev[0], 0);
+    }
     if (e == hipSuccess)
         e = hipMalloc(&f->LA, sizeof(float) * (size_t)(ntA * (ntA + 1) / 2) * bk::TILE_ELEMS);
-    if (e == hipSuccess)
-        e = bk::factor_one(stream, A, n, (double)damp, Z, Ninv, T, scal, flags,
-                           reinterpret_cast<int64_t*>(flags) + 2, f->LA, ntA);
     if (e == hipSuccess && B) {
         const int64_t mtB = cdiv(m, bk::TS);
         f->LB_tiles = mtB;
         e = hipMalloc(&f->LB, sizeof(float) * (size_t)(mtB * (mtB + 1) / 2) * bk::TILE_ELEMS);
         if (e == hipSuccess)
-            e = bk::factor_one(stream, B, m, (double)damp, Z, Ninv, T, scal + 1, flags + 1,
+            e = bk::factor_one(sB, B, m, (double)damp, Z[1], Ninv[1], T[1], scal + 1, flags + 1,
                                reinterpret_cast<int64_t*>(flags) + 3, f->LB, mtB);
+    }
+    if (e == hipSuccess)
+        e = bk::factor_one(stream, A, n, (double)damp, Z[0], Ninv[0], T[0], scal, flags,
+                           reinterpret_cast<int64_t*>(flags) + 2, f->LA, ntA);
+    if (e == hipSuccess && B) {
+        e = hipEventRecord(ev[1], sB);
+        if (e == hipSuccess) e = hipStreamWaitEvent(stream, ev[1], 0);
     }
     if (e != hipSuccess) {
         st = hip_fail(&g_last_error, e, "bakron_factor: launch");
+        if (sB) (void)hipStreamSynchronize(sB);
         cleanup();
         bakron_factors_free(f);
         return st;
