@@ -123,9 +123,10 @@ bakron_status bakron_factor(const float *A, int64_t n, const float *B, int64_t m
  * solve may fork onto two streams of the handle, restricted to disjoint CU
  * sets (the divide-and-conquer pushes into later segments overlap with the
  * segment launches), and joins back into `stream` with events; on the legacy
- * default stream, which synchronises implicitly with such streams, and with
- * the environment variable BAKRON_DEFER=0, everything runs on `stream`.  The
- * results are bitwise the same either way.  Kernel faults surface as
+ * default stream, which synchronises implicitly with such streams, with
+ * the environment variable BAKRON_DEFER=0, and while `stream` is being
+ * captured into a graph, everything runs on `stream`.  The results are
+ * bitwise the same either way.  Kernel faults surface as
  * BAKRON_EHIP on a later call or at the caller's synchronisation.
  */
 bakron_status bakron_solve(const float *W, int64_t m, int64_t n, const bakron_factors *f,

@@ -622,7 +622,11 @@ static bakron_status solve_impl(const float* W, int64_t m, int64_t n, const bakr
     // the legacy default stream synchronises implicitly with the (blocking)
     // CU-restricted streams, so calls on it use the one-stream plan
     const bool legacy = stream == nullptr || stream == hipStreamLegacy;
-    const int pi = (!legacy && !f->plan[1].side.empty()) ? 1 : 0;
+    // under stream capture all launches stay on the capturing stream (the
+    // two-stream fork is not captured)
+    hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+    if (!legacy && hipStreamIsCapturing(stream, &cap) != hipSuccess) cap = hipStreamCaptureStatusNone;
+    const int pi = (!legacy && cap == hipStreamCaptureStatusNone && !f->plan[1].side.empty()) ? 1 : 0;
     f->last_plan = pi;
     hipEvent_t* tim = nullptr;
     f->prof_valid = 0;
