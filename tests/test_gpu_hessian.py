@@ -252,3 +252,60 @@ def test_power_step_one_is_single_shampoo():
         nb, st), a.device)
     torch.cuda.synchronize()
     assert torch.equal(A1, A2) and torch.equal(B1, B2)
+
+
+def _sampled_pairs(rng, d, k=40):
+    pr = [(int(i), int(j)) for i, j in rng.integers(0, d, (k, 2))]
+    return pr + [(i, i) for i in rng.integers(0, d, 8).tolist()]
+
+
+@pytest.mark.parametrize("workload", ["global-kfac", "global-shampoo", "mlp-local-kfac"])
+def test_factors_full_size_sampled(oracle_mod, workload):
+    """bench.py --factors' launch configuration at the paper's calibration size
+    (256 x 2048 samples): 48 entries of each factor against the oracle's
+    per-entry means, within the summation bound of each entry."""
+    import torch
+    import paper_2608_06291_amd as pk
+    h = oracle_mod.hessian
+    N = 256 * 2048
+    dev = torch.device("cuda:0")
+    log(f"case full-size factors {workload} N={N}")
+    rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([4200, len(workload)])))
+    if workload.startswith("global"):
+        p = workloads.kron_samples_torch(N, 4096, 4096, 0, dev)
+        a, b, D = p["a"], p["b"], None
+        style = workload.split("-")[1]
+        A, B = pk.kron_factors(a, b, style)
+    else:
+        p = workloads.mlp_samples_torch(N, 4096, 14336, 0, dev, "g")
+        a, b, D = p["x"], p["feat"], p["Wd"]
+        style = "kfac"
+        A, B = pk.mlp_local_factors(a, b, D, style)
+    torch.cuda.synchronize()
+    for X, F, wsrc, mask, lab in ((a, A, b, None, "A"), (b, B, a, D, "B")):
+        d = X.shape[1]
+        pr = _sampled_pairs(rng, d)
+        idx = sorted({i for q in pr for i in q})
+        cols = X[:, idx].double().cpu().numpy()
+        pos = {c: t for t, c in enumerate(idx)}
+        q = [(pos[i], pos[j]) for i, j in pr]
+        w = None
+        if style == "shampoo":   # |other sample|^2 as the weight, fp64 on the CPU
+            w = np.empty(N)
+            for k0 in range(0, N, 65536):
+                blk = wsrc[k0:k0 + 65536].double()
+                w[k0:k0 + 65536] = (blk * blk).sum(1).cpu().numpy()
+        expect = h.expect_outer_entries(cols, q, w)
+        absum = h.expect_outer_entries(np.abs(cols), q, None if w is None else np.abs(w))
+        if mask is not None:
+            dcols = mask[:, idx].double().cpu().numpy()
+            m_e = mask.shape[0] * h.expect_outer_entries(dcols, q)
+            m_a = mask.shape[0] * h.expect_outer_entries(np.abs(dcols), q)
+            expect, absum = expect * m_e, absum * np.abs(m_a)
+        got = np.array([F[i, j].item() for i, j in pr])
+        bound = (N + 2 * d + 8) * U32 * absum
+        worst = float(np.max(np.abs(got - expect) / (bound + 1e-30)))
+        log(f"[full {workload}] {lab} max err/bound {worst:.3e}")
+        assert worst <= 1.0, (workload, lab)
+    del a, b, D, A, B, p
+    torch.cuda.empty_cache()
