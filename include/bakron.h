@@ -61,7 +61,9 @@ typedef enum {
  *   s_ij = base_ij * (col_scale ? col_scale[j] : 1)     (one fp32 product)
  *   base_ij = group_size > 0 ? scale[i * ceil(n / group_size) + j / group_size]
  *                            : scale[i]
- * All scales are >= 0; s_ij = 0 makes the entry's alphabet {0}.  The caller
+ * All scales must be finite and >= 0 (not checked on the device: a negative
+ * scale acts as 0, a NaN scale gives NaN in V); s_ij = 0 makes the entry's
+ * alphabet {0}.  The caller
  * chooses the scales (App. D: max_j |W_ij| / l per row, optionally shrunk by
  * an MSE search: bakron_mse_scales).
  *   bits        alphabet size, in [2, 8]
@@ -200,6 +202,11 @@ bakron_status bakron_factor_blockdiag(const float *A, int64_t n, const float *B_
 bakron_status bakron_mse_scales(const float *W, int64_t m, int64_t n, int32_t bits,
                                 int32_t alphabet, int32_t group_size, int32_t grid,
                                 double maxshrink, float *scale, hipStream_t stream);
+
+/* Debug aid: with the environment variable BAKRON_POISON=1 when a handle is
+ * created, every solve on it first fills the whole solve workspace with
+ * NaN / -1 bytes (an extra launch); the results are unchanged, which shows
+ * that no workspace word is read before the solve writes it. */
 
 /* Frees the handle, its factors and its workspace (synchronises the device
  * work that used them).  NULL is a no-op. */

@@ -43,6 +43,11 @@ struct bakron_factors {
     void* ws_mem = nullptr;         // X, Y tile arrays, flags, counters, status (bk::Workspace)
     bk::Workspace ws{};
     int knear = 8;
+    // BAKRON_POISON=1 at creation: fill the workspace with NaN / -1 before
+    // every solve (debug aid: the solve must never read a word it did not
+    // write first)
+    int poison = 0;
+    size_t ws_bytes = 0;
     // plan[0]: everything on the caller's stream; plan[1]: with side ops
     // (empty if the side stream is not used).  Both make the same additions
     // to every tile in the same order, so their results are identical.
@@ -306,6 +311,7 @@ extern "C" bakron_status bakron_factor(const float* A, int64_t n, const float* B
     f->m = B ? m : 0;
     f->b_ident = B ? 0 : 1;
     f->damp = damp;
+    if (const char* pz = std::getenv("BAKRON_POISON")) f->poison = std::atoi(pz) != 0;
     if (const char* kn = std::getenv("BAKRON_KNEAR")) {
         int v = std::atoi(kn);
         if (v >= 0 && v <= bk::KNEAR_MAX) f->knear = v;
@@ -532,6 +538,7 @@ static bakron_status ensure_workspace(bakron_factors* f, int64_t m, int64_t n) {
     const size_t ibytes = sizeof(int) * (tiles + (size_t)f->plan[0].nseg + 1);
     hipError_t e = hipMalloc(&f->ws_mem, 2 * fbytes + ibytes);
     if (e != hipSuccess) return hip_fail(&f->err, e, "bakron_solve: hipMalloc (workspace)");
+    f->ws_bytes = 2 * fbytes + ibytes;
     char* base = static_cast<char*>(f->ws_mem);
     int* ints = reinterpret_cast<int*>(base + 2 * fbytes);
     f->ws = bk::Workspace{reinterpret_cast<float*>(base), reinterpret_cast<float*>(base + fbytes),
@@ -645,7 +652,8 @@ static bakron_status solve_impl(const float* W, int64_t m, int64_t n, const bakr
     const bool fork = pi == 1;
     hipStream_t ms = fork ? f->main : stream;
     hipError_t e = hipSuccess;
-    if (fork) {
+    if (f->poison) e = bk::fill_words(stream, f->ws_mem, (int64_t)(f->ws_bytes / 4), 0xFFFFFFFFu);
+    if (fork && e == hipSuccess) {
         e = hipEventRecord(f->ev_fork, stream);
         if (e == hipSuccess) e = hipStreamWaitEvent(ms, f->ev_fork, 0);
     }
@@ -702,6 +710,11 @@ extern "C" bakron_status bakron_solve_antidiag(const float* W, int64_t m, int64_
         if (e != hipSuccess) return hip_fail(&f->err, e, "bakron_solve_antidiag: hipMalloc (workspace)");
         f->ad_m = m;
         f->ad_n = n;
+    }
+    if (f->poison) {
+        const size_t elems = (size_t)cdiv(m * n, 64) * 64 + (size_t)(cdiv(m, bk::TS) * bk::TS);
+        hipError_t pe = bk::fill_words(stream, f->ad_mem, (int64_t)elems, 0xFFFFFFFFu);
+        if (pe != hipSuccess) return hip_fail(&f->err, pe, "bakron_solve_antidiag: poison");
     }
     hipError_t e = bk::run_antidiag(stream, W, m, n, f->ad_mem, f->ad_mem + (size_t)cdiv(m * n, 64) * 64, f->LA,
                                     f->LB, quant_args(q, n), codes, V, pre);

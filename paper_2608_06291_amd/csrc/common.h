@@ -134,6 +134,9 @@ __device__ inline float row_scale_of(const QuantArgs& q, int64_t row, const ColS
     return q.scale[row * (q.gsize > 0 ? q.ngroups : 1) + c.goff] * c.cf;
 }
 
+// Fills n 32-bit words at p with v on stream st (debug poisoning).
+hipError_t fill_words(hipStream_t st, void* p, int64_t n, uint32_t v);
+
 // Records the message returned by bakron_last_error() for this thread.
 void set_last_error(const char* msg);
 

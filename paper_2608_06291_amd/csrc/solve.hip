@@ -31,6 +31,8 @@
 // tiles with per-tile ready flags); node products take only pairs farther
 // apart than KNEAR, so each (source, target) tile pair is applied exactly
 // once.
+#include <algorithm>
+
 #include "common.h"
 
 #include <vector>
@@ -504,6 +506,20 @@ __global__ __launch_bounds__(512) void k_seg(SegArgs a) {
             }
         }
     }
+}
+
+// Fills n 32-bit words with v (a debug aid: poisoning the workspace before a
+// solve shows that every word the solve reads was written by it first).
+__global__ __launch_bounds__(256) void k_fill_u32(uint32_t* __restrict__ p, int64_t n, uint32_t v) {
+    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256)
+        p[i] = v;
+}
+
+hipError_t fill_words(hipStream_t st, void* p, int64_t n, uint32_t v) {
+    if (n <= 0) return hipSuccess;
+    const int64_t g = std::min<int64_t>((n + 255) / 256, 65536);
+    hipLaunchKernelGGL(k_fill_u32, dim3((unsigned)g), dim3(256), 0, st, static_cast<uint32_t*>(p), n, v);
+    return hipGetLastError();
 }
 
 struct NodeArgs {

@@ -5,7 +5,7 @@ import numpy as np
 import pytest
 
 import workloads
-from gpu_util import check_against_oracle, gpu_run, log
+from gpu_util import check_against_oracle, gpu_run, gpu_run_antidiag, log
 
 pytestmark = pytest.mark.gpu
 
@@ -124,3 +124,32 @@ def test_side_stream_bitwise(m, n, k):
         assert np.array_equal(c0, c)
         assert np.array_equal(v0.view(np.uint32), v.view(np.uint32))
         assert np.array_equal(x0.view(np.uint32), x.view(np.uint32))
+
+
+@pytest.mark.parametrize("m,n,k,identity_B", [(257, 129, None, False), (100, 97, 0, False),
+                                               (130, 70, 3, True)])
+def test_poisoned_workspace_bitwise(m, n, k, identity_B):
+    """With BAKRON_POISON=1 the handle fills its whole workspace with NaN / -1
+    bytes before every solve; the results must equal an unpoisoned solve bit
+    for bit (no word of the workspace is read before the solve writes it)."""
+    import os
+    p = workloads.make_random(m, n, seed=404, identity_B=identity_B)
+    log(f"case poisoned workspace m={m} n={n} k={k} B=I={identity_B}")
+    ref = gpu_run(p, k=k)
+    old = os.environ.get("BAKRON_POISON")
+    os.environ["BAKRON_POISON"] = "1"
+    try:
+        got = gpu_run(p, k=k, repeat=2)
+        ad = gpu_run_antidiag(p)
+    finally:
+        if old is None:
+            del os.environ["BAKRON_POISON"]
+        else:
+            os.environ["BAKRON_POISON"] = old
+    for c, v, x in got:
+        assert np.array_equal(c, ref[0])
+        assert np.array_equal(v.view(np.uint32), ref[1].view(np.uint32))
+        assert np.array_equal(np.isnan(x), np.isnan(ref[2]))
+    ref_ad = gpu_run_antidiag(p)
+    assert np.array_equal(ad[0], ref_ad[0]) and np.array_equal(ad[1].view(np.uint32),
+                                                               ref_ad[1].view(np.uint32))
