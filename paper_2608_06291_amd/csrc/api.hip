@@ -8,8 +8,12 @@
 #include <cstdlib>
 #include <cstring>
 #include <algorithm>
+#include <map>
+#include <memory>
+#include <mutex>
 #include <new>
 #include <string>
+#include <tuple>
 #include <vector>
 
 namespace bk {
@@ -53,8 +57,7 @@ struct bakron_factors {
     // to every tile in the same order, so their results are identical.
     bk::Plan plan[2];
     int last_plan = 0;
-    std::vector<int4> items_host;   // node work lists of both plans
-    int4* items = nullptr;
+    const int4* items = nullptr;    // device copy, owned by the process-wide plan cache
     // measurement hook: per timed launch (enqueue order) its class and work
     int prof = 0;
     int prof_valid = 0;
@@ -424,13 +427,11 @@ extern "C" void bakron_factors_free(bakron_factors* f) {
     if (f->LB) hipFree(f->LB);
     if (f->ws_mem) hipFree(f->ws_mem);
     if (f->ad_mem) hipFree(f->ad_mem);
-    if (f->side) hipStreamDestroy(f->side);
-    if (f->main) hipStreamDestroy(f->main);
+    // f->side, f->main and f->items belong to the process-wide plan cache
     if (f->ev_fork) hipEventDestroy(f->ev_fork);
     if (f->ev_join) hipEventDestroy(f->ev_join);
     for (hipEvent_t ev : f->ev_rel) hipEventDestroy(ev);
     for (hipEvent_t ev : f->ev_side) hipEventDestroy(ev);
-    if (f->items) hipFree(f->items);
     for (hipEvent_t ev : f->tim) hipEventDestroy(ev);
     if (cur != f->device) hipSetDevice(cur);
     delete f;
@@ -455,46 +456,114 @@ static bakron_status ensure_identity(bakron_factors* f, int64_t mt) {
 // [R, #CUs) with R = max(#CUs / 2, widest segment rounded up to 32), when at
 // least 64 CUs remain.  BAKRON_DEFER=0 keeps every push on the caller's
 // stream, and so does a failure to create the side stream.
-static bakron_status plan_with_side_stream(bakron_factors* f, int mt, int nt) {
-    build_plan(mt, nt, f->knear, f->b_ident, false, f->plan[0], f->items_host);
-    f->plan[1] = bk::Plan{};
-    const char* env = std::getenv("BAKRON_DEFER");
-    if (env && std::atoi(env) == 0) return BAKRON_OK;
+// Launch plans, their node work lists on the device and the two CU-restricted
+// streams depend only on the device and the solve shape, so they are built
+// once per process and shared by every handle (read-only; kept until the
+// process ends).  Handles that fork onto the same streams concurrently are
+// serialised on them, which keeps each solve's ordering intact.
+struct PlanEntry {
+    bk::Plan plan[2];
+    const int4* items = nullptr;
+    hipStream_t main = nullptr, side = nullptr;
+};
+static std::mutex g_plan_mu;
+static std::map<std::tuple<int, int, int, int, int, int>, std::shared_ptr<PlanEntry>> g_plans;
+static std::map<std::pair<int, int>, std::pair<hipStream_t, hipStream_t>> g_streams;
+
+// main ops on CUs [0, R), side ops on [R, #CUs): a persistent segment
+// workgroup never sits on a CU a side push waits for, and the reverse
+static bool masked_streams(int device, int ncu, int R, hipStream_t* main, hipStream_t* side) {
+    auto it = g_streams.find({device, R});
+    if (it != g_streams.end()) {
+        *main = it->second.first;
+        *side = it->second.second;
+        return true;
+    }
+    auto masked = [&](int lo, int hi, hipStream_t* out) {
+        std::vector<uint32_t> mask((size_t)(ncu + 31) / 32, 0u);
+        for (int c = lo; c < hi; ++c) mask[(size_t)c / 32] |= 1u << (c % 32);
+        if (hipExtStreamCreateWithCUMask(out, (uint32_t)mask.size(), mask.data()) != hipSuccess ||
+            !*out) {
+            *out = nullptr;
+            (void)hipGetLastError();
+            return false;
+        }
+        return true;
+    };
+    hipStream_t m = nullptr, sd = nullptr;
+    if (!masked(0, R, &m) || !masked(R, ncu, &sd)) {
+        if (m) (void)hipStreamDestroy(m);
+        return false;
+    }
+    g_streams[{device, R}] = {m, sd};
+    *main = m;
+    *side = sd;
+    return true;
+}
+
+static bakron_status build_plan_entry(bakron_factors* f, int mt, int nt, bool defer_on,
+                                      PlanEntry& pe) {
+    std::vector<int4> items_host;
+    build_plan(mt, nt, f->knear, f->b_ident, false, pe.plan[0], items_host);
+    pe.plan[1] = bk::Plan{};
+    int ncu = 0;
     hipDeviceProp_t prop;
-    if (hipGetDeviceProperties(&prop, f->device) != hipSuccess) return BAKRON_OK;
-    const int ncu = prop.multiProcessorCount;
+    if (defer_on && hipGetDeviceProperties(&prop, f->device) == hipSuccess) ncu = prop.multiProcessorCount;
     int widest = 0;
-    for (const bk::PlanOp& op : f->plan[0].ops)
+    for (const bk::PlanOp& op : pe.plan[0].ops)
         if (op.kind == 0) widest = imax(widest, op.nstrips);
     const int R = imax(ncu / 2, (widest + 31) / 32 * 32);
-    if (ncu - R < 64) return BAKRON_OK;
-    if (!f->side || f->side_cu_lo != R) {
-        for (hipStream_t* ps : {&f->side, &f->main})
-            if (*ps) {
-                (void)hipStreamSynchronize(*ps);
-                (void)hipStreamDestroy(*ps);
-                *ps = nullptr;
-            }
-        f->side_cu_lo = -1;
-        // main ops on CUs [0, R), side ops on [R, #CUs): a persistent segment
-        // workgroup never sits on a CU a side push waits for, and the reverse
-        auto masked = [&](int lo, int hi, hipStream_t* out) {
-            std::vector<uint32_t> mask((size_t)(ncu + 31) / 32, 0u);
-            for (int c = lo; c < hi; ++c) mask[(size_t)c / 32] |= 1u << (c % 32);
-            if (hipExtStreamCreateWithCUMask(out, (uint32_t)mask.size(), mask.data()) != hipSuccess ||
-                !*out) {
-                *out = nullptr;
-                (void)hipGetLastError();
-                return false;
-            }
-            return true;
-        };
-        if (!masked(0, R, &f->main) || !masked(R, ncu, &f->side)) {
-            if (f->main) { (void)hipStreamDestroy(f->main); f->main = nullptr; }
-            return BAKRON_OK;   // no side stream: every push stays on the caller's stream
+    if (ncu > 0 && ncu - R >= 64 && masked_streams(f->device, ncu, R, &pe.main, &pe.side)) {
+        bk::Plan deferred;
+        std::vector<int4> items;
+        build_plan(mt, nt, f->knear, f->b_ident, true, deferred, items);
+        deferred.side_cu_lo = R;
+        if (!deferred.side.empty()) {
+            const int off = (int)items_host.size();
+            for (bk::PlanOp& op : deferred.ops) if (op.kind == 1) op.item_off += off;
+            for (bk::PlanOp& op : deferred.side) op.item_off += off;
+            items_host.insert(items_host.end(), items.begin(), items.end());
+            pe.plan[1] = std::move(deferred);
         }
-        f->side_cu_lo = R;
     }
+    if (!items_host.empty()) {
+        int4* dev = nullptr;
+        const size_t ib = sizeof(int4) * items_host.size();
+        hipError_t e = hipMalloc(&dev, ib);
+        if (e == hipSuccess) e = hipMemcpy(dev, items_host.data(), ib, hipMemcpyHostToDevice);
+        if (e != hipSuccess) {
+            if (dev) hipFree(dev);
+            return hip_fail(&f->err, e, "bakron_solve: work list upload");
+        }
+        pe.items = dev;
+    }
+    return BAKRON_OK;
+}
+
+static bakron_status plan_with_side_stream(bakron_factors* f, int mt, int nt) {
+    const char* env = std::getenv("BAKRON_DEFER");
+    const int defer_on = (env && std::atoi(env) == 0) ? 0 : 1;
+    const auto key = std::make_tuple(f->device, mt, nt, f->knear, f->b_ident, defer_on);
+    std::shared_ptr<PlanEntry> pe;
+    {
+        std::lock_guard<std::mutex> lock(g_plan_mu);
+        auto it = g_plans.find(key);
+        if (it != g_plans.end()) {
+            pe = it->second;
+        } else {
+            pe = std::make_shared<PlanEntry>();
+            bakron_status st = build_plan_entry(f, mt, nt, defer_on != 0, *pe);
+            if (st != BAKRON_OK) return st;
+            g_plans[key] = pe;
+        }
+    }
+    f->plan[0] = pe->plan[0];
+    f->plan[1] = pe->plan[1];
+    f->items = pe->items;
+    f->main = pe->main;
+    f->side = pe->side;
+    f->side_cu_lo = pe->plan[1].side.empty() ? -1 : pe->plan[1].side_cu_lo;
+    if (pe->plan[1].side.empty()) return BAKRON_OK;
     auto grow = [](std::vector<hipEvent_t>& v, size_t need) {
         while (v.size() < need) {
             hipEvent_t ev;
@@ -504,24 +573,11 @@ static bakron_status plan_with_side_stream(bakron_factors* f, int mt, int nt) {
         return true;
     };
     if ((!f->ev_fork && hipEventCreateWithFlags(&f->ev_fork, hipEventDisableTiming) != hipSuccess) ||
-        (!f->ev_join && hipEventCreateWithFlags(&f->ev_join, hipEventDisableTiming) != hipSuccess)) {
+        (!f->ev_join && hipEventCreateWithFlags(&f->ev_join, hipEventDisableTiming) != hipSuccess) ||
+        !grow(f->ev_rel, f->plan[1].ops.size()) || !grow(f->ev_side, f->plan[1].side.size())) {
         (void)hipGetLastError();
-        return BAKRON_OK;
+        f->plan[1] = bk::Plan{};   // no events: every push stays on the caller's stream
     }
-    bk::Plan deferred;
-    std::vector<int4> items;
-    build_plan(mt, nt, f->knear, f->b_ident, true, deferred, items);
-    if (!grow(f->ev_rel, deferred.ops.size()) || !grow(f->ev_side, deferred.side.size())) {
-        (void)hipGetLastError();
-        return BAKRON_OK;
-    }
-    deferred.side_cu_lo = R;
-    if (deferred.side.empty()) return BAKRON_OK;
-    const int off = (int)f->items_host.size();
-    for (bk::PlanOp& op : deferred.ops) if (op.kind == 1) op.item_off += off;
-    for (bk::PlanOp& op : deferred.side) op.item_off += off;
-    f->items_host.insert(f->items_host.end(), items.begin(), items.end());
-    f->plan[1] = std::move(deferred);
     return BAKRON_OK;
 }
 
@@ -545,13 +601,6 @@ static bakron_status ensure_workspace(bakron_factors* f, int64_t m, int64_t n) {
                           ints, ints + tiles, ints + tiles + f->plan[0].nseg};
     st = ensure_identity(f, mt);
     if (st != BAKRON_OK) return st;
-    if (f->items) { hipFree(f->items); f->items = nullptr; }
-    if (!f->items_host.empty()) {
-        const size_t ib = sizeof(int4) * f->items_host.size();
-        e = hipMalloc(&f->items, ib);
-        if (e == hipSuccess) e = hipMemcpy(f->items, f->items_host.data(), ib, hipMemcpyHostToDevice);
-        if (e != hipSuccess) return hip_fail(&f->err, e, "bakron_solve: work list upload");
-    }
     // per timed launch: class and work, in plan order
     for (int pi = 0; pi < 2; ++pi) {
         const bk::Plan& pl = f->plan[pi];
