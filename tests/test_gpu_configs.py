@@ -92,3 +92,36 @@ def test_config2_two_stream_plan_bitwise():
     assert np.array_equal(c0, c1)
     assert np.array_equal(v0.view(np.uint32), v1.view(np.uint32))
     assert np.array_equal(x0.view(np.uint32), x1.view(np.uint32))
+
+
+@pytest.mark.timeout(900)
+def test_config2_general_quantiser_certificate(oracle_mod):
+    """The 4096 x 4096 layer with the general quantiser (asymmetric INT4
+    alphabet, MSE-searched 128-column group scales, per-column factors), at
+    full size on a stream of its own: the closed-form certificate on sampled
+    rows with per-entry scales."""
+    import torch
+    import paper_2608_06291_amd as pk
+    o = oracle_mod
+    log("case config 2 general quantiser: generating")
+    c = workloads.make(2, seed=0, device="cuda")
+    m, n = c["W"].shape
+    # the scales: the GPU search is itself checked against the oracle's
+    # elsewhere; here the oracle's own search provides them
+    scale, _ = o.mse_scales(c["W"], 4, "asym", group_size=128)
+    col = np.random.Generator(np.random.PCG64(77)).uniform(0.8, 1.25, n).astype(np.float32)
+    p = dict(c, scale=scale, alphabet="asym", group_size=128, col_scale=col)
+    log("case config 2 general quantiser: solving")
+    codes, V, pre = _run(p, True)
+    S = o.entry_scales(scale, m, n, group_size=128, col_scale=col)
+    assert v_is_scale_times_code(V, codes, S)
+    assert np.all((codes >= -8) & (codes <= 7))
+    rows = _rows(m, full=False)
+    x = o.certificate(c["W"], c["A"], c["B"], c["damp"], S, codes, 4, rows=rows)
+    v = o.verdict(codes[rows], x, 4, window=TIE_WINDOW, alphabet="asym")
+    fin = np.isfinite(x)
+    margin = float(np.max(np.abs(pre[rows][fin].astype(np.float64) - x[fin])))
+    log(f"[config2-general] {v} margin={margin:.3e}")
+    assert v["violations"] == 0
+    assert v["flips"] <= MAX_FLIP_RATE * v["total"]
+    del torch, pk
