@@ -124,9 +124,12 @@ bakron_status bakron_factor(const float *A, int64_t n, const float *B, int64_t m
  * On a stream other than the legacy default stream (0 / hipStreamLegacy) the
  * solve may fork onto two streams of the handle, restricted to disjoint CU
  * sets (the divide-and-conquer pushes into later segments overlap with the
- * segment launches), and joins back into `stream` with events; on the legacy
- * default stream, which synchronises implicitly with such streams, with
- * the environment variable BAKRON_DEFER=0, and while `stream` is being
+ * segment launches), and joins back into `stream` with events.  It does so
+ * for the shapes where a cost model of both schedules, built when the shape
+ * is first planned, favours the overlap (near-square layers up to about
+ * 4096 x 4096), always with the environment variable BAKRON_DEFER=1, and
+ * never with BAKRON_DEFER=0.  On the legacy default stream, which
+ * synchronises implicitly with such streams, and while `stream` is being
  * captured into a graph, everything runs on `stream`.  The results are
  * bitwise the same either way.  Kernel faults surface as
  * BAKRON_EHIP on a later call or at the caller's synchronisation.

@@ -501,24 +501,67 @@ static bool masked_streams(int device, int ncu, int R, hipStream_t* main, hipStr
     return true;
 }
 
-static bakron_status build_plan_entry(bakron_factors* f, int mt, int nt, bool defer_on,
+// Modelled duration of a plan (seconds): main ops in order, side ops in
+// order, a side op starting after the main op it is released by, a main op
+// after the side ops it waits for, each wait across the two streams adding
+// a fixed latency.  A segment costs a fixed time per tile anti-diagonal (its
+// sequential chain); a node push a fixed launch cost plus its MFMA flops at
+// a per-CU rate on the CUs of its stream, a side push a larger fixed cost.
+// The constants are fitted to MI355X solve times of twelve layer shapes
+// (3072^2 to 14336 x 4096) under both plans; only the comparison of the two
+// plans for one shape uses them.
+static double plan_model_seconds(const bk::Plan& p, int cus_main, int cus_side) {
+    const double t_diag = 14.2e-6, t_seg = 3e-6, t_node = 6e-6, t_side = 30e-6, t_wait = 40e-6;
+    const double rate_cu = 0.45e12;
+    std::vector<double> main_end(p.ops.size(), 0.0), side_end(p.side.size(), 0.0);
+    double tm = 0.0, ts = 0.0;
+    size_t next_side = 0;
+    auto run_side = [&](size_t upto) {
+        for (; next_side < upto; ++next_side) {
+            const bk::PlanOp& o = p.side[next_side];
+            ts = std::max(ts, main_end[o.rel] + t_wait) + t_side +
+                 o.mfma_flops / (rate_cu * cus_side);
+            side_end[next_side] = ts;
+        }
+    };
+    for (size_t i = 0; i < p.ops.size(); ++i) {
+        const bk::PlanOp& o = p.ops[i];
+        run_side((size_t)o.need_side);
+        if (o.need_side > 0) tm = std::max(tm, side_end[o.need_side - 1] + t_wait);
+        tm += o.kind == 0 ? t_seg + (o.L - o.K) * t_diag
+                          : t_node + o.mfma_flops / (rate_cu * cus_main);
+        main_end[i] = tm;
+    }
+    run_side(p.side.size());
+    return std::max(tm, ts);
+}
+
+// defer: 0 never, 1 whenever enough CUs are free, 2 when the modelled
+// duration of the two-stream plan is below that of the one-stream plan
+static bakron_status build_plan_entry(bakron_factors* f, int mt, int nt, int defer,
                                       PlanEntry& pe) {
     std::vector<int4> items_host;
     build_plan(mt, nt, f->knear, f->b_ident, false, pe.plan[0], items_host);
     pe.plan[1] = bk::Plan{};
     int ncu = 0;
     hipDeviceProp_t prop;
-    if (defer_on && hipGetDeviceProperties(&prop, f->device) == hipSuccess) ncu = prop.multiProcessorCount;
+    if (defer && hipGetDeviceProperties(&prop, f->device) == hipSuccess) ncu = prop.multiProcessorCount;
     int widest = 0;
     for (const bk::PlanOp& op : pe.plan[0].ops)
         if (op.kind == 0) widest = imax(widest, op.nstrips);
     const int R = imax(ncu / 2, (widest + 31) / 32 * 32);
-    if (ncu > 0 && ncu - R >= 64 && masked_streams(f->device, ncu, R, &pe.main, &pe.side)) {
+    if (ncu > 0 && ncu - R >= 64) {
         bk::Plan deferred;
         std::vector<int4> items;
         build_plan(mt, nt, f->knear, f->b_ident, true, deferred, items);
         deferred.side_cu_lo = R;
-        if (!deferred.side.empty()) {
+        // the overlap pays only while the pushes into later segments fit on
+        // the side CUs during the chain; with more push work (tall or wide
+        // layers) one stream with every CU per push is faster
+        const bool use = !deferred.side.empty() &&
+                         (defer == 1 || plan_model_seconds(deferred, R, ncu - R) <
+                                            plan_model_seconds(pe.plan[0], ncu, 0));
+        if (use && masked_streams(f->device, ncu, R, &pe.main, &pe.side)) {
             const int off = (int)items_host.size();
             for (bk::PlanOp& op : deferred.ops) if (op.kind == 1) op.item_off += off;
             for (bk::PlanOp& op : deferred.side) op.item_off += off;
@@ -542,8 +585,8 @@ static bakron_status build_plan_entry(bakron_factors* f, int mt, int nt, bool de
 
 static bakron_status plan_with_side_stream(bakron_factors* f, int mt, int nt) {
     const char* env = std::getenv("BAKRON_DEFER");
-    const int defer_on = (env && std::atoi(env) == 0) ? 0 : 1;
-    const auto key = std::make_tuple(f->device, mt, nt, f->knear, f->b_ident, defer_on);
+    const int defer = env ? (std::atoi(env) == 0 ? 0 : 1) : 2;
+    const auto key = std::make_tuple(f->device, mt, nt, f->knear, f->b_ident, defer);
     std::shared_ptr<PlanEntry> pe;
     {
         std::lock_guard<std::mutex> lock(g_plan_mu);
@@ -552,7 +595,7 @@ static bakron_status plan_with_side_stream(bakron_factors* f, int mt, int nt) {
             pe = it->second;
         } else {
             pe = std::make_shared<PlanEntry>();
-            bakron_status st = build_plan_entry(f, mt, nt, defer_on != 0, *pe);
+            bakron_status st = build_plan_entry(f, mt, nt, defer, *pe);
             if (st != BAKRON_OK) return st;
             g_plans[key] = pe;
         }
