@@ -18,6 +18,7 @@
 namespace bk {
 
 constexpr int NB = 64;  // factor block
+constexpr int NB2 = 256;  // Cholesky panel (multiple of NB)
 
 // ---------------------------------------------------------------------------
 __global__ void k_diag_mean(const float* __restrict__ X, int64_t d, double* __restrict__ mean) {
@@ -165,6 +166,9 @@ __global__ __launch_bounds__(NB) void k_inv_lower_blocks(const double* __restric
 // D[l / 16 + 4 r][l % 16]).
 // op(B) = B (K x N, ldb) or B^T (B is N x K, ldb).  lower_only skips output
 // blocks lying entirely above the diagonal (row index < col index) of C.
+// tri: bit 0 = A is lower triangular (A[i][k] = 0 for k > i), bit 1 = op(B)
+// is lower triangular (op(B)[k][j] = 0 for k < j); the K loop of a block then
+// skips the chunks that only meet those zeros.
 // One workgroup per 64 x 64 block of C, 4 waves of 2 x 2 MFMA blocks; K in
 // chunks of 16 staged through double-buffered LDS as [k][row] / [k][col],
 // the next chunk loaded into registers while the current one is multiplied.
@@ -174,11 +178,14 @@ __global__ __launch_bounds__(256) void k_gemm64(int64_t M, int64_t N, int64_t K,
                                                 const double* __restrict__ A, int64_t lda,
                                                 const double* __restrict__ B, int64_t ldb,
                                                 int transB, double beta, double* __restrict__ C,
-                                                int64_t ldc, int lower_only,
+                                                int64_t ldc, int lower_only, int tri,
                                                 const int* __restrict__ fail) {
     if (*fail) return;
     const int64_t r0 = (int64_t)blockIdx.y * GB, c0 = (int64_t)blockIdx.x * GB;
     if (lower_only && c0 > r0 + GB - 1) return;
+    // K range that can hold nonzero products for this block (GK-aligned start)
+    const int64_t kbeg = (tri & 2) ? (c0 < K ? c0 / GK * GK : K) : 0;
+    const int64_t kend = (tri & 1) ? (r0 + GB < K ? r0 + GB : K) : K;
     __shared__ double As[2][GK][GPAD];
     __shared__ double Bs[2][GK][GPAD];
     const int t = threadIdx.x;
@@ -226,16 +233,16 @@ __global__ __launch_bounds__(256) void k_gemm64(int64_t M, int64_t N, int64_t K,
     for (int x = 0; x < 2; ++x)
 #pragma unroll
         for (int y = 0; y < 2; ++y) acc[x][y] = f64x4{0.0, 0.0, 0.0, 0.0};
-    const int64_t nch = (K + GK - 1) / GK;
+    const int64_t nch = kend > kbeg ? (kend - kbeg + GK - 1) / GK : 0;
     if (nch > 0) {
-        load(0);
+        load(kbeg);
         store(0);
     }
     __syncthreads();
     for (int64_t c = 0; c < nch; ++c) {
         const int sb = (int)(c & 1);
         const bool more = c + 1 < nch;
-        if (more) load((c + 1) * GK);
+        if (more) load(kbeg + (c + 1) * GK);
 #pragma unroll
         for (int kk = 0; kk < GK / 4; ++kk) {
             const int kr = 4 * kk + lk;
@@ -347,11 +354,12 @@ static inline unsigned grid1d(int64_t total, int threads = 256) {
 
 static hipError_t gemm64(hipStream_t s, int64_t M, int64_t N, int64_t K, double alpha,
                          const double* A, int64_t lda, const double* B, int64_t ldb, int transB,
-                         double beta, double* C, int64_t ldc, int lower, const int* fail) {
+                         double beta, double* C, int64_t ldc, int lower, const int* fail,
+                         int tri = 0) {
     if (M <= 0 || N <= 0) return hipSuccess;
     dim3 grid((unsigned)((N + GB - 1) / GB), (unsigned)((M + GB - 1) / GB));
     hipLaunchKernelGGL(k_gemm64, grid, dim3(256), 0, s, M, N, K, alpha, A, lda, B, ldb, transB,
-                       beta, C, ldc, lower, fail);
+                       beta, C, ldc, lower, tri, fail);
     return hipGetLastError();
 }
 
@@ -368,13 +376,13 @@ static hipError_t trtri_rec(hipStream_t s, const double* C, double* Ninv, int64_
     e = trtri_rec(s, C, Ninv, ld, off + h, sz - h, T, fail);
     if (e != hipSuccess) return e;
     const int64_t n2 = sz - h;
-    // T (n2 x h) = C21 * N11
+    // T (n2 x h) = C21 * N11 (N11 lower triangular)
     e = gemm64(s, n2, h, h, 1.0, C + (off + h) * ld + off, ld, Ninv + off * ld + off, ld, 0, 0.0, T,
-               h, 0, fail);
+               h, 0, fail, 2);
     if (e != hipSuccess) return e;
-    // N21 = -N22 * T
+    // N21 = -N22 * T (N22 lower triangular)
     return gemm64(s, n2, h, n2, -1.0, Ninv + (off + h) * ld + (off + h), ld, T, h, 0, 0.0,
-                  Ninv + (off + h) * ld + off, ld, 0, fail);
+                  Ninv + (off + h) * ld + off, ld, 0, fail, 1);
 }
 
 // Factor one matrix.  Z, Ninv: d*d doubles; T: d*d/4 + d*NB doubles;
@@ -386,17 +394,32 @@ hipError_t factor_one(hipStream_t s, const float* X, int64_t d, double lam, doub
     hipLaunchKernelGGL(k_flip_damp, dim3(grid1d(d * d)), dim3(256), 0, s, X, d, mean, lam, Z);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    for (int64_t k0 = 0; k0 < d; k0 += NB) {
-        const int b = (int)((d - k0) < NB ? (d - k0) : NB);
-        hipLaunchKernelGGL(k_potrf_diag, dim3(1), dim3(NB), 0, s, Z, d, k0, b, fail, fail_pivot);
-        const int64_t rest = d - k0 - b;
+    // Two-level right-looking Cholesky: panels of NB2 columns, each factored
+    // in NB-column steps (diagonal block, substitution for every row below,
+    // update of the panel's remaining columns), then one rank-NB2 update of
+    // the trailing matrix, which reads and writes it NB2 / NB times less
+    // often than rank-NB updates would.
+    for (int64_t p0 = 0; p0 < d; p0 += NB2) {
+        const int64_t pend = (d - p0) < NB2 ? d : p0 + NB2;
+        for (int64_t k0 = p0; k0 < pend; k0 += NB) {
+            const int b = (int)((pend - k0) < NB ? (pend - k0) : NB);
+            hipLaunchKernelGGL(k_potrf_diag, dim3(1), dim3(NB), 0, s, Z, d, k0, b, fail, fail_pivot);
+            const int64_t rest = d - k0 - b;
+            if (rest > 0) {
+                // panel solve: P <- P C_kk^-T by substitution
+                hipLaunchKernelGGL(k_trsm_panel, dim3((unsigned)((rest + 255) / 256)), dim3(256), 0,
+                                   s, Z, d, k0, b, rest, fail);
+                // the panel's remaining columns: Z[k0+b:, k0+b:pend] -= P P[k0+b:pend]^T
+                e = gemm64(s, rest, pend - k0 - b, b, -1.0, Z + (k0 + b) * d + k0, d,
+                           Z + (k0 + b) * d + k0, d, 1, 1.0, Z + (k0 + b) * d + (k0 + b), d, 1, fail);
+                if (e != hipSuccess) return e;
+            }
+        }
+        const int64_t rest = d - pend;
         if (rest > 0) {
-            // panel solve: P <- P C_kk^-T by substitution
-            hipLaunchKernelGGL(k_trsm_panel, dim3((unsigned)((rest + 255) / 256)), dim3(256), 0, s, Z,
-                               d, k0, b, rest, fail);
-            // trailing update Z22 -= P P^T (lower blocks)
-            e = gemm64(s, rest, rest, b, -1.0, Z + (k0 + b) * d + k0, d, Z + (k0 + b) * d + k0, d, 1,
-                       1.0, Z + (k0 + b) * d + (k0 + b), d, 1, fail);
+            // trailing update Z22 -= P P^T over the whole panel (lower blocks)
+            e = gemm64(s, rest, rest, pend - p0, -1.0, Z + pend * d + p0, d, Z + pend * d + p0, d, 1,
+                       1.0, Z + pend * d + pend, d, 1, fail);
             if (e != hipSuccess) return e;
         }
     }
