@@ -52,8 +52,11 @@ __global__ void k_flip_damp(const float* __restrict__ X, int64_t d, const double
 // only), one wave: lane i holds row i of the block in registers; column j is
 // finished by lane j's pivot (read by every lane through LDS), scaled in each
 // lane, published to LDS and used by every later row for its trailing
-// update.  LDS operations of one wave complete in order, so no barrier is
-// needed.  A non-positive or non-finite pivot sets *fail and records the
+// update.  The update runs over every column right of j in every lane, with
+// the multiplier zeroed in lanes above the diagonal (i < j): entries right of
+// a lane's diagonal then hold bounded values that are never read or stored,
+// and no instruction is predicated per entry.  LDS operations of one wave
+// complete in order, so no barrier is needed.  A non-positive or non-finite pivot sets *fail and records the
 // pivot index in the reversed ordering.
 __global__ __launch_bounds__(NB) void k_potrf_diag(double* __restrict__ Z, int64_t ld, int64_t k0,
                                                    int b, int* __restrict__ fail,
@@ -83,9 +86,9 @@ __global__ __launch_bounds__(NB) void k_potrf_diag(double* __restrict__ Z, int64
         __builtin_amdgcn_wave_barrier();
         col[i] = row[j];                                     // column j of the factor (rows > j)
         __builtin_amdgcn_wave_barrier();
+        const double mj = (j <= i) ? row[j] : 0.0;
 #pragma unroll
-        for (int c = j + 1; c < NB; ++c)
-            if (c <= i) row[c] = fma(-row[j], col[c], row[c]);
+        for (int c = j + 1; c < NB; ++c) row[c] = fma(-mj, col[c], row[c]);
         __builtin_amdgcn_wave_barrier();
     }
     if (i < b) {
@@ -98,16 +101,21 @@ __global__ __launch_bounds__(NB) void k_potrf_diag(double* __restrict__ Z, int64
 // Panel of the blocked Cholesky: every row r >= k0 + b of Z[:, k0:k0+b] is
 // replaced by the solution x of x C_kk^T = Z[r, k0:k0+b] (C_kk the factored
 // diagonal block, lower): x_j = (p_j - sum_{c<j} x_c C_jc) / C_jj, one thread
-// per row, C_kk in LDS (read as broadcasts), x in registers.
+// per row, C_kk and the reciprocals of its diagonal in LDS (read as
+// broadcasts), x in registers; each sum is split over four accumulators to
+// shorten the dependent FMA chain.
 __global__ __launch_bounds__(256) void k_trsm_panel(double* __restrict__ Z, int64_t ld, int64_t k0,
                                                     int b, int64_t rows,
                                                     const int* __restrict__ fail) {
     if (*fail) return;
     __shared__ double Ck[NB][NB + 1];
+    __shared__ double rdiag[NB];
     for (int e = threadIdx.x; e < NB * NB; e += 256) {
         const int i = e / NB, c = e % NB;
         Ck[i][c] = (i < b && c <= i) ? Z[(k0 + i) * ld + (k0 + c)] : 0.0;
     }
+    if (threadIdx.x < NB)
+        rdiag[threadIdx.x] = (int)threadIdx.x < b ? 1.0 / Z[(k0 + threadIdx.x) * ld + (k0 + threadIdx.x)] : 0.0;
     __syncthreads();
     const int64_t r = (int64_t)blockIdx.x * 256 + threadIdx.x;
     if (r >= rows) return;
@@ -115,10 +123,10 @@ __global__ __launch_bounds__(256) void k_trsm_panel(double* __restrict__ Z, int6
     double x[NB];
 #pragma unroll
     for (int j = 0; j < NB; ++j) {
-        double v = j < b ? p[j] : 0.0;
+        double a[4] = {j < b ? p[j] : 0.0, 0.0, 0.0, 0.0};
 #pragma unroll
-        for (int c = 0; c < j; ++c) v = fma(-x[c], Ck[j][c], v);
-        x[j] = j < b ? v / Ck[j][j] : 0.0;
+        for (int c = 0; c < j; ++c) a[c & 3] = fma(-x[c], Ck[j][c], a[c & 3]);
+        x[j] = j < b ? ((a[0] + a[1]) + (a[2] + a[3])) * rdiag[j] : 0.0;
     }
 #pragma unroll
     for (int j = 0; j < NB; ++j)
