@@ -470,6 +470,23 @@ static std::mutex g_plan_mu;
 static std::map<std::tuple<int, int, int, int, int, int>, std::shared_ptr<PlanEntry>> g_plans;
 static std::map<std::pair<int, int>, std::pair<hipStream_t, hipStream_t>> g_streams;
 
+// At process exit (registered once, after the HIP runtime has initialised, so
+// it runs before the runtime's own teardown): destroy the cached streams and
+// free the device work lists, so that no CU-restricted queue outlives the
+// program's last call.
+static void release_plan_cache() {
+    std::lock_guard<std::mutex> lock(g_plan_mu);
+    for (auto& kv : g_streams) {
+        (void)hipStreamDestroy(kv.second.first);
+        (void)hipStreamDestroy(kv.second.second);
+    }
+    g_streams.clear();
+    for (auto& kv : g_plans)
+        if (kv.second->items) (void)hipFree(const_cast<int4*>(kv.second->items));
+    g_plans.clear();
+    (void)hipGetLastError();
+}
+
 // main ops on CUs [0, R), side ops on [R, #CUs): a persistent segment
 // workgroup never sits on a CU a side push waits for, and the reverse
 static bool masked_streams(int device, int ncu, int R, hipStream_t* main, hipStream_t* side) {
@@ -597,6 +614,8 @@ static bakron_status plan_with_side_stream(bakron_factors* f, int mt, int nt) {
             pe = std::make_shared<PlanEntry>();
             bakron_status st = build_plan_entry(f, mt, nt, defer, *pe);
             if (st != BAKRON_OK) return st;
+            static const bool registered = std::atexit(release_plan_cache) == 0;
+            (void)registered;
             g_plans[key] = pe;
         }
     }
