@@ -93,6 +93,17 @@ int main() {
     for (auto& sh : small) for (int k : {0, 1, 3, 8}) for (int bi : {0, 1}) for (int d : {0, 1})
         fails += check(sh[0], sh[1], k, bi, d);
     for (int k : {1, 8}) for (int d : {0, 1}) fails += check(128, 128, k, 0, d);   // the 4096^2 layer
+    // the cost model's choice on 256 CUs, as measured on MI355X: the overlap
+    // for the 4096^2 layer (main CUs 0-127), one stream for 11008 x 4096
+    // and 8192 x 2048 (overlap 1.7x and 1.6x slower)
+    int shapes[3][3] = {{128, 128, 1}, {344, 128, 0}, {256, 64, 0}};
+    for (auto& sh : shapes) {
+        bk::Plan p0, p1; std::vector<int4> it;
+        build_plan(sh[0], sh[1], 8, 0, false, p0, it);
+        build_plan(sh[0], sh[1], 8, 0, true, p1, it);
+        const bool two = plan_model_seconds(p1, 128, 128) < plan_model_seconds(p0, 256, 0);
+        if (two != (sh[2] != 0)) { printf("cost model picks the wrong plan for %dx%d tiles\n", sh[0], sh[1]); ++fails; }
+    }
     printf("fails %d\n", fails);
     return fails;
 }
