@@ -657,6 +657,12 @@ def main():
     # the segment launches carry the sequential chain: per tile anti-diagonal
     n_diag = (m + 31) // 32 + (n + 31) // 32 - 1
     seg["us_per_tile_diagonal"] = seg["ms_per_step"] * 1e3 / n_diag
+    # wavefront bandwidth: HBM bytes per launch (rocprofv3 counters, while the
+    # kernel source is unchanged) over the live average launch duration
+    seg_traffic = measured_traffic("k_seg", cfg.name)
+    if seg_traffic is not None and seg["avg_launch_us"] > 0:
+        seg["hbm_gbps"] = seg_traffic / (seg["avg_launch_us"] * 1e-6) / 1e9
+        seg["hbm_frac"] = seg["hbm_gbps"] / PEAK_HBM
     # dominant kernel class: the segment launches carry the sequential chain on
     # the solve's critical path (node pushes into later segments overlap with
     # them on a side stream), so they bound the step unless node launches take
@@ -665,8 +671,7 @@ def main():
     if dominant == "segment":
         roof = dict(kernel="k_seg (persistent tile-wavefront rounding with near-field pulls)",
                     bound="alu", achieved=tf["segment"], peak=PEAK_FP32_VALU, unit="TFLOP/s",
-                    frac=tf["segment"] / PEAK_FP32_VALU,
-                    traffic=measured_traffic("k_seg", cfg.name))
+                    frac=tf["segment"] / PEAK_FP32_VALU, traffic=seg_traffic)
     else:
         roof = dict(kernel="k_node (divide-and-conquer band push), fp32 MFMA", bound="mfma",
                     achieved=tf["node"], peak=PEAK_FP32_MFMA, unit="TFLOP/s",
