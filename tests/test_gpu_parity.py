@@ -95,14 +95,15 @@ def test_ar1_structured_exact(oracle_mod):
     assert r["n_flip"] <= 1e-4 * m * n
 
 
-@pytest.mark.parametrize("m,n,k", [(600, 500, 8), (300, 420, 1)])
+@pytest.mark.parametrize("m,n,k", [(600, 500, 8), (300, 420, 1), (1100, 300, 8), (300, 1100, 8)])
 def test_side_stream_bitwise(m, n, k):
-    """On a non-default stream, node pushes into later segments run on a
-    CU-restricted side stream (BAKRON_DEFER, read when a handle first plans a
-    shape); on the legacy default stream and with BAKRON_DEFER=0 everything
-    runs on the caller's stream.  Every target tile receives the same
-    additions in the same order either way, so the results must be bitwise
-    identical."""
+    """On a non-default stream with BAKRON_DEFER=1 (read when a handle first
+    plans a shape), node pushes into later segments run on a CU-restricted
+    side stream, also on the tall and wide shapes where the cost model would
+    keep one stream; on the legacy default stream and with BAKRON_DEFER=0
+    everything runs on the caller's stream.  Every target tile receives the
+    same additions in the same order either way, so the results must be
+    bitwise identical."""
     import os
     import torch
     p = _problem(m, n, seed=m + 3 * n)
