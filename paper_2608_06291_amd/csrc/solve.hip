@@ -683,6 +683,7 @@ __global__ __launch_bounds__(256, (MT == 4 ? 2 : 4)) void k_node(NodeArgs a) {
 // ready flags <- 0 and ticket counters <- 0.  One workgroup per tile; the
 // transpose goes through LDS so that both the read of W and the write of X
 // are coalesced.
+template <bool VEC>
 __global__ __launch_bounds__(256) void k_prep(const float* __restrict__ W, int64_t m, int64_t n,
                                               int mt, int nt, float* __restrict__ X,
                                               float* __restrict__ Y, int* __restrict__ flags,
@@ -692,21 +693,39 @@ __global__ __launch_bounds__(256) void k_prep(const float* __restrict__ W, int64
     const int64_t tile = blockIdx.x;
     const int64_t I = tile / nt, J = tile - (tile / nt) * nt;
     const int tid = threadIdx.x;
-#pragma unroll
-    for (int k = 0; k < TILE_ELEMS / 256; ++k) {
-        const int e = k * 256 + tid;
-        const int r = e >> 5, c = e & 31;
-        const int64_t gr = I * TS + r, gc = J * TS + c;
-        T[r][c] = (gr < m && gc < n) ? W[gr * n + gc] : 0.0f;
-    }
-    __syncthreads();
     const int64_t base = tile * TILE_ELEMS;
+    if (VEC) {
+        // W rows as 16-byte chunks (n % 4 == 0, W 16-byte aligned), one per
+        // thread; X (the tile transposed) and Y as contiguous 16-byte stores
+        const int r = tid >> 3, c4 = (tid & 7) * 4;
+        const int64_t gr = I * TS + r, gc = J * TS + c4;
+        float4 v = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+        if (gr < m && gc < n) v = *reinterpret_cast<const float4*>(W + gr * n + gc);
+        T[r][c4] = v.x;
+        T[r][c4 + 1] = v.y;
+        T[r][c4 + 2] = v.z;
+        T[r][c4 + 3] = v.w;
+        __syncthreads();
+        const int c = tid >> 3, r4 = (tid & 7) * 4;
+        *reinterpret_cast<float4*>(X + base + 4 * tid) =
+            make_float4(T[r4][c], T[r4 + 1][c], T[r4 + 2][c], T[r4 + 3][c]);
+        *reinterpret_cast<float4*>(Y + base + 4 * tid) = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+    } else {
 #pragma unroll
-    for (int k = 0; k < TILE_ELEMS / 256; ++k) {
-        const int e = k * 256 + tid;
-        const int c = e >> 5, r = e & 31;
-        X[base + e] = T[r][c];
-        Y[base + e] = 0.0f;
+        for (int k = 0; k < TILE_ELEMS / 256; ++k) {
+            const int e = k * 256 + tid;
+            const int r = e >> 5, c = e & 31;
+            const int64_t gr = I * TS + r, gc = J * TS + c;
+            T[r][c] = (gr < m && gc < n) ? W[gr * n + gc] : 0.0f;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int k = 0; k < TILE_ELEMS / 256; ++k) {
+            const int e = k * 256 + tid;
+            const int c = e >> 5, r = e & 31;
+            X[base + e] = T[r][c];
+            Y[base + e] = 0.0f;
+        }
     }
     if (tid == 0) flags[tile] = 0;
     if (tile == 0) {
@@ -732,8 +751,12 @@ hipError_t run_plan(hipStream_t st, hipStream_t side, const Plan& plan, const fl
     auto t_end = [&](hipStream_t s) { if (tim) (void)hipEventRecord(tim[2 * ti + 1], s); ++ti; };
     hipError_t e;
     t_begin(st);
-    hipLaunchKernelGGL(k_prep, dim3((unsigned)((int64_t)mt * nt)), dim3(256), 0, st, W, m, n, mt, nt,
-                       ws.X, ws.Y, ws.flags, ws.counters, plan.nseg, ws.status);
+    if (n % 4 == 0 && reinterpret_cast<uintptr_t>(W) % 16 == 0)
+        hipLaunchKernelGGL(k_prep<true>, dim3((unsigned)((int64_t)mt * nt)), dim3(256), 0, st, W, m,
+                           n, mt, nt, ws.X, ws.Y, ws.flags, ws.counters, plan.nseg, ws.status);
+    else
+        hipLaunchKernelGGL(k_prep<false>, dim3((unsigned)((int64_t)mt * nt)), dim3(256), 0, st, W, m,
+                           n, mt, nt, ws.X, ws.Y, ws.flags, ws.counters, plan.nseg, ws.status);
     t_end(st);
     if ((e = hipGetLastError()) != hipSuccess) return e;
 
