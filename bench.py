@@ -25,6 +25,7 @@ METRIC = "BaKron solve ms/layer and TFLOP/s (fraction of fp32 MFMA peak), 1 MI35
 PEAK_FP32_MFMA = 157.3      # TFLOP/s, 256 CU x 4 SIMD x 64 flop/clk x 2.4 GHz
 PEAK_FP32_VALU = 157.3      # TFLOP/s, 256 CU x 256 flop/clk x 2.4 GHz (packed dual-issue)
 PEAK_HBM = 8000.0           # GB/s
+PEAK_FP64_MFMA = 78.6       # TFLOP/s, dense fp64 matrix peak
 # Paper, Table 3: 4096 x 4096 solved in 0.288 s on one RTX PRO 6000 (fp32).
 PAPER_4096_S = 0.288
 # Paper, Table 3 (seconds on one RTX PRO 6000, fp32): (m, n): (GPTQ, BaKron, BaKron-antidiagonal)
@@ -433,6 +434,43 @@ def quant_bench(steps: int):
         log(f"[quant] {r}")
 
 
+def factorise_bench(dims, steps: int):
+    """bakron_factor alone on two d x d factors (damping, reverse Cholesky,
+    triangular inverse and packing; A and B concurrently), inputs
+    the AR(1) Toeplitz matrices rho^|i-j| (rho 0.5 / 0.2) resident in HBM.
+    Counted fp64 work 4 d^3 / 3 (d^3 / 3 for each Cholesky and each inverse).
+    One JSON line per d."""
+    import torch
+    import paper_2608_06291_amd as pk
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.Stream(dev)
+    torch.cuda.set_stream(stream)
+    for d in dims:
+        i = torch.arange(d, device=dev, dtype=torch.float32)
+        A = 0.5 ** (i[:, None] - i[None, :]).abs()
+        B = 0.2 ** (i[:, None] - i[None, :]).abs()
+        del i
+        pk.factor(A, B, 0.01).close()            # warm-up: scratch allocation, clocks
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(steps):
+            t0 = time.perf_counter()
+            f = pk.factor(A, B, 0.01)
+            torch.cuda.synchronize()
+            ts.append((time.perf_counter() - t0) * 1e3)
+            f.close()
+        ms = sorted(ts)[len(ts) // 2]
+        flops = 4.0 * d ** 3 / 3.0
+        tf = flops / (ms * 1e-3) / 1e12
+        print(json.dumps({"metric": "bakron_factor ms (A and B, d x d each, concurrently)",
+                          "value": ms, "unit": "ms", "higher_is_better": False, "d": d,
+                          "steps": steps, "counted_fp64_tflop": flops / 1e12,
+                          "fp64_tflops": tf, "frac_fp64_mfma_peak": tf / PEAK_FP64_MFMA,
+                          "data": "synthetic"}), flush=True)
+        del A, B
+        torch.cuda.empty_cache()
+
+
 def flow_bench(L: int, d: int, N: int, style: str):
     """Sec. 5's recursive flow over a stack of L square layers (width d, N
     calibration samples, SiLU): per phase, the summed device time of the
@@ -534,6 +572,9 @@ def main():
     ap.add_argument("--quant", action="store_true",
                     help="only time the quantiser variants and the MSE scale search on the "
                          "4096 x 4096 layer and exit")
+    ap.add_argument("--factorise", default=None, metavar="d[,d...]",
+                    help="time bakron_factor alone on d x d factor pairs (damping, reverse "
+                         "Cholesky, triangular inverse)")
     ap.add_argument("--flow", default=None, metavar="L,d,N[,style]",
                     help="only run the recursive backprop flow (Sec. 5) over L layers of width d "
                          "with N samples (style kfac or shampooK) and exit")
@@ -559,6 +600,9 @@ def main():
         quant_bench(args.steps)
         return
 
+    if args.factorise:
+        factorise_bench([int(x) for x in args.factorise.split(",")], max(args.steps, 1))
+        return
     if args.flow:
         parts = args.flow.split(",")
         flow_bench(int(parts[0]), int(parts[1]), int(parts[2]), parts[3] if len(parts) > 3 else "kfac")
