@@ -130,7 +130,10 @@ bakron_status bakron_factor(const float *A, int64_t n, const float *B, int64_t m
  * 4096 x 4096), always with the environment variable BAKRON_DEFER=1, and
  * never with BAKRON_DEFER=0.  On the legacy default stream, which
  * synchronises implicitly with such streams, and while `stream` is being
- * captured into a graph, everything runs on `stream`.  The results are
+ * captured into a graph, everything runs on `stream`.  Unless
+ * BAKRON_DEFER=0, the first solve planned on a device creates the two
+ * CU-restricted streams, whichever plan its shape uses; the library keeps
+ * them, with the launch plans, until the process exits.  The results are
  * bitwise the same either way.  Kernel faults surface as
  * BAKRON_EHIP on a later call or at the caller's synchronisation.
  */
