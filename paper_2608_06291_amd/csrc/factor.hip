@@ -18,7 +18,7 @@
 namespace bk {
 
 constexpr int NB = 64;  // factor block
-constexpr int NB2 = 256;  // Cholesky panel (multiple of NB)
+constexpr int NB2 = 512;  // Cholesky panel (multiple of NB)
 
 // ---------------------------------------------------------------------------
 __global__ void k_diag_mean(const float* __restrict__ X, int64_t d, double* __restrict__ mean) {
