@@ -35,17 +35,25 @@ def test_quantiser_ties_clamp_zero_scale(oracle_mod):
 
 
 # ---------------------------------------------------------------- golden
-@pytest.mark.parametrize("name", ["hand_2x2_ar1.json", "hand_1x3_clamp.json"])
+@pytest.mark.parametrize("name", ["hand_2x2_ar1.json", "hand_1x3_clamp.json",
+                                  "hand_2x2_damp.json"])
 def test_hand_worked_examples(oracle_mod, name):
+    o = oracle_mod
     g = json.load(open(os.path.join(GOLDEN, name)))
     W = np.array(g["W"], np.float64)
-    r = oracle_mod.solve(W, np.array(g["A"]), np.array(g["B"]), g["damp"],
-                         np.array(g["scale"]), g["bits"])
+    r = o.solve(W, np.array(g["A"]), np.array(g["B"]), g["damp"], np.array(g["scale"]), g["bits"])
     assert r["codes"].tolist() == g["codes"]
     np.testing.assert_allclose(r["pre"], np.array(g["pre"]), atol=1e-12)
     if "L" in g:
-        np.testing.assert_allclose(oracle_mod.normalized_factor(np.array(g["A"]), 0.0),
+        np.testing.assert_allclose(o.normalized_factor(np.array(g["A"]), 0.0),
                                    np.array(g["L"]), atol=1e-14)
+    # damping with each factor's own mean diagonal, and the factors it leads to
+    for X, key, lkey in (("A", "Ad", "LA"), ("B", "Bd", "LB")):
+        if key in g:
+            np.testing.assert_allclose(o.damp(np.array(g[X]), g["damp"]), np.array(g[key]),
+                                       rtol=0, atol=1e-15)
+            np.testing.assert_allclose(o.normalized_factor(np.array(g[X]), g["damp"]),
+                                       np.array(g[lkey]), rtol=0, atol=1e-15)
 
 
 # ---------------------------------------------------------------- brute force
@@ -152,23 +160,29 @@ def test_diagonal_hessians_give_round_to_nearest(oracle_mod):
 
 
 def test_fine_grid_returns_W(oracle_mod):
-    """Corollary 3.4 (no clamping): a grid much finer than W's spread gives V ~ W, with
-    |V - W|_max <= (s/2) max_p |L^B_p,:|_1 max_q |L^A_q,:|_1 (V - W0 = L^B E L^A^T)."""
+    """North-star check 3 (Eq. (1) with Cor. 3.4's no-clamping premise): with one
+    scale s for every row and a grid fine enough that nothing clamps, every
+    error obeys |E| <= s/2, so V - W0 = L^B E L^A^T gives
+    |V - W|_max <= (s/2) max_p |L^B_p,:|_1 max_q |L^A_q,:|_1 -> 0 with s."""
     o = oracle_mod
-    p = _rand_problem(24, 20, seed=11, bits=8)
+    m, n = 24, 20
+    p = _rand_problem(m, n, seed=11, bits=8)
     W = p["W"].astype(np.float64)
-    s = 1e-4
     LA = o.normalized_factor(p["A"], p["damp"])
     LB = o.normalized_factor(p["B"], p["damp"])
-    r = o.babai(W, LA, LB, np.full(24, s), 8)
-    assert np.max(np.abs(r["codes"])) < 127 or True
-    bound = 0.5 * s * np.max(np.abs(LB).sum(1)) * np.max(np.abs(LA).sum(1))
-    unclamped = np.all(np.abs(r["pre"]) < 127.5)
-    if unclamped:
-        assert np.max(np.abs(r["V"] - W)) <= bound * (1 + 1e-9)
-    # coarse-vs-fine: error shrinks with s
-    r2 = o.babai(W, LA, LB, np.full(24, s / 16), 8)
-    assert np.max(np.abs(r2["V"] - W)) < np.max(np.abs(r["V"] - W)) or not unclamped
+    growth = np.max(np.abs(LB).sum(1)) * np.max(np.abs(LA).sum(1))
+    s0 = np.max(np.abs(W)) / 100.0         # finest grid: |W|/s <= 100 inside the INT8 range
+    errs = []
+    for s in (64 * s0, 16 * s0, 4 * s0, s0):
+        r = o.babai(W, LA, LB, np.full(m, s), 8)
+        # the premise: no entry clamps (|x| < l + 1/2 = 127.5), so |E| <= s/2
+        assert np.max(np.abs(r["pre"])) < 127.5
+        assert np.max(np.abs(r["V"] - r["pre"] * s)) <= 0.5 * s * (1 + 1e-12)
+        err = np.max(np.abs(r["V"] - W))
+        assert err <= 0.5 * s * growth * (1 + 1e-9)
+        errs.append(err)
+    # V -> W: the error falls with the grid step
+    assert errs[0] > errs[1] > errs[2] > errs[3]
 
 
 def test_error_bound_cor34(oracle_mod):
