@@ -61,9 +61,11 @@ typedef enum {
  *   s_ij = base_ij * (col_scale ? col_scale[j] : 1)     (one fp32 product)
  *   base_ij = group_size > 0 ? scale[i * ceil(n / group_size) + j / group_size]
  *                            : scale[i]
- * All scales must be finite and >= 0 (not checked on the device: a negative
- * scale acts as 0, a NaN scale gives NaN in V); s_ij = 0 makes the entry's
- * alphabet {0}.  The caller
+ * All scales must be finite and >= 0.  bakron_solve_debug checks this and
+ * returns BAKRON_EINVAL otherwise; bakron_solve does not look (a device
+ * reduction plus a synchronisation would break its asynchrony): there a
+ * negative scale acts as 0 and a NaN scale gives NaN in V.  s_ij = 0 makes the
+ * entry's alphabet {0}.  The caller
  * chooses the scales (App. D: max_j |W_ij| / l per row, optionally shrunk by
  * an MSE search: bakron_mse_scales).
  *   bits        alphabet size, in [2, 8]
@@ -145,6 +147,10 @@ bakron_status bakron_solve(const float *W, int64_t m, int64_t n, const bakron_fa
  * pre-rounding value in grid units x_ij = W~_ij / s_ij (device, m x n fp32;
  * NaN where s_ij = 0), the value at which the entry was quantised.
  * Used to measure the numerical margin against the fp64 oracle.
+ * Before enqueuing the solve it validates the quantiser's scales on the device
+ * (every scale, and every col_scale factor, finite and >= 0) and synchronises
+ * `stream` once to read the result: BAKRON_EINVAL (nothing else enqueued) if
+ * one is negative, NaN or infinite.  Not capturable into a graph.
  */
 bakron_status bakron_solve_debug(const float *W, int64_t m, int64_t n, const bakron_factors *f,
                                  bakron_quantizer q, int8_t *codes, float *V, float *pre,
@@ -210,9 +216,12 @@ bakron_status bakron_mse_scales(const float *W, int64_t m, int64_t n, int32_t bi
                                 double maxshrink, float *scale, hipStream_t stream);
 
 /* Debug aid: with the environment variable BAKRON_POISON=1 when a handle is
- * created, every solve on it first fills the whole solve workspace with
- * NaN / -1 bytes (an extra launch); the results are unchanged, which shows
- * that no workspace word is read before the solve writes it. */
+ * created, every solve on it first fills the whole solve workspace (except the
+ * sticky status word of bakron_solve_check) with NaN / -1 bytes (an extra
+ * launch); the results are unchanged, which shows that no workspace word is
+ * read before the solve writes it.  BAKRON_SPIN_LIMIT=k (1 <= k <= 2^22),
+ * read at every solve, lowers the number of polls after which a tile-ordering
+ * wait gives up, to exercise that path (bakron_solve_check) from the host. */
 
 /* Frees the handle, its factors and its workspace (synchronises the device
  * work that used them).  NULL is a no-op. */
@@ -269,9 +278,13 @@ bakron_status bakron_profile_read(const bakron_factors *f, bakron_kernel_stat *s
 /*
  * bakron_solve_check -- diagnostic (not needed for solving; synchronises
  * `stream`).  The solve orders the tiles inside one launch with bounded
- * waits on per-tile ready flags; *failed receives 1 if a wait of the last
- * solve gave up (its output is then invalid), else 0.  A correct run never
- * gives up: every awaited tile is held by a running workgroup.
+ * waits on per-tile ready flags.  *failed receives 1 if a wait gave up in any
+ * solve on this handle since the last check (or since the workspace for the
+ * current shape was created), else 0; the record is then cleared.  The record
+ * is sticky on the device: once a wait has given up, every wait of every later
+ * solve returns at once, so all outputs since the failure are invalid.  A
+ * correct run never gives up: every awaited tile is held by a running
+ * workgroup.
  */
 bakron_status bakron_solve_check(const bakron_factors *f, hipStream_t stream, int32_t *failed);
 

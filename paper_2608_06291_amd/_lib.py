@@ -177,8 +177,9 @@ class Factors:
         return {k: arr[i].as_dict() for i, k in enumerate(self.PROFILE_CLASSES)}
 
     def check(self) -> bool:
-        """True if the last solve on the current stream completed every
-        ordered wait (synchronises the stream)."""
+        """True if every solve on this handle since the last check completed
+        all of its ordered waits (synchronises the current stream; a give-up
+        record is sticky on the device until this call clears it)."""
         import torch
         failed = ctypes.c_int32(0)
         st = load().bakron_solve_check(self._h, _stream(torch, self.device), ctypes.byref(failed))

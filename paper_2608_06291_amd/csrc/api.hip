@@ -27,8 +27,9 @@ hipError_t unpack_factor(hipStream_t s, const float* packed, int64_t d, float* d
 hipError_t run_plan(hipStream_t st, hipStream_t side, const Plan& plan, const float* W, int64_t m,
                     int64_t n, int mt, int nt, const Workspace& ws, const float* LA, const float* LB,
                     int b_ident, const QuantArgs& q, int8_t* codes, float* V, float* pre,
-                    int knear, const int4* items, hipEvent_t* tim, hipEvent_t* ev_rel,
-                    hipEvent_t* ev_side);
+                    int knear, int spin_limit, const int4* items, hipEvent_t* tim,
+                    hipEvent_t* ev_rel, hipEvent_t* ev_side);
+hipError_t check_scales(hipStream_t st, const float* s, int64_t count, int* bad);
 int plan_timed_launches(const Plan& plan);
 hipError_t run_antidiag(hipStream_t st, const float* W, int64_t m, int64_t n, float* Wt,
                         float* delta, const float* LA, const float* LB, const QuantArgs& q,
@@ -674,14 +675,19 @@ static bakron_status ensure_workspace(bakron_factors* f, int64_t m, int64_t n) {
     if (st != BAKRON_OK) return st;
     const size_t tiles = (size_t)mt * (size_t)nt;
     const size_t fbytes = sizeof(float) * tiles * bk::TILE_ELEMS;
-    const size_t ibytes = sizeof(int) * (tiles + (size_t)f->plan[0].nseg + 1);
+    const size_t ibytes = sizeof(int) * (tiles + (size_t)f->plan[0].nseg + 2);
     hipError_t e = hipMalloc(&f->ws_mem, 2 * fbytes + ibytes);
     if (e != hipSuccess) return hip_fail(&f->err, e, "bakron_solve: hipMalloc (workspace)");
     f->ws_bytes = 2 * fbytes + ibytes;
     char* base = static_cast<char*>(f->ws_mem);
     int* ints = reinterpret_cast<int*>(base + 2 * fbytes);
+    int* st_words = ints + tiles + f->plan[0].nseg;   // status, scale_bad: the last two words
     f->ws = bk::Workspace{reinterpret_cast<float*>(base), reinterpret_cast<float*>(base + fbytes),
-                          ints, ints + tiles, ints + tiles + f->plan[0].nseg};
+                          ints, ints + tiles, st_words, st_words + 1};
+    // the give-up status is cleared here and by bakron_solve_check only
+    e = hipMemset(st_words, 0, 2 * sizeof(int));
+    if (e == hipSuccess) e = hipDeviceSynchronize();
+    if (e != hipSuccess) return hip_fail(&f->err, e, "bakron_solve: workspace status init");
     st = ensure_identity(f, mt);
     if (st != BAKRON_OK) return st;
     // per timed launch: class and work, in plan order
@@ -758,6 +764,30 @@ static bakron_status solve_impl(const float* W, int64_t m, int64_t n, const bakr
     if (st != BAKRON_OK) return st;
     const int mt = (int)cdiv(m, bk::TS), nt = (int)cdiv(n, bk::TS);
     const bk::QuantArgs qa = quant_args(q, n);
+    if (pre) {
+        // debug mode: every scale must be finite and >= 0 (a device reduction,
+        // then one synchronisation of `stream`)
+        const int64_t ns = m * (int64_t)qa.ngroups;
+        int32_t bad = 0;
+        hipError_t ce = hipMemsetAsync(f->ws.scale_bad, 0, sizeof(int), stream);
+        if (ce == hipSuccess) ce = bk::check_scales(stream, q.scale, ns, f->ws.scale_bad);
+        if (ce == hipSuccess && q.col_scale) ce = bk::check_scales(stream, q.col_scale, n, f->ws.scale_bad);
+        if (ce == hipSuccess)
+            ce = hipMemcpyAsync(&bad, f->ws.scale_bad, sizeof(bad), hipMemcpyDeviceToHost, stream);
+        if (ce == hipSuccess) ce = hipStreamSynchronize(stream);
+        if (ce != hipSuccess) return hip_fail(&f->err, ce, "bakron_solve_debug: scale check");
+        if (bad) {
+            f->err = "bakron_solve_debug: a scale is negative, NaN or infinite";
+            return BAKRON_EINVAL;
+        }
+    }
+    // polls before a tile-ordering wait gives up; BAKRON_SPIN_LIMIT (read at
+    // every solve) lowers it, to exercise the give-up path from the host
+    int spin_limit = bk::SPIN_LIMIT;
+    if (const char* sl = std::getenv("BAKRON_SPIN_LIMIT")) {
+        const int v = std::atoi(sl);
+        if (v >= 1 && v <= bk::SPIN_LIMIT) spin_limit = v;
+    }
     // the legacy default stream synchronises implicitly with the (blocking)
     // CU-restricted streams, so calls on it use the one-stream plan
     const bool legacy = stream == nullptr || stream == hipStreamLegacy;
@@ -784,15 +814,16 @@ static bakron_status solve_impl(const float* W, int64_t m, int64_t n, const bakr
     const bool fork = pi == 1;
     hipStream_t ms = fork ? f->main : stream;
     hipError_t e = hipSuccess;
-    if (f->poison) e = bk::fill_words(stream, f->ws_mem, (int64_t)(f->ws_bytes / 4), 0xFFFFFFFFu);
+    // poisoning spares the last two words (the sticky status and the scale flag)
+    if (f->poison) e = bk::fill_words(stream, f->ws_mem, (int64_t)(f->ws_bytes / 4) - 2, 0xFFFFFFFFu);
     if (fork && e == hipSuccess) {
         e = hipEventRecord(f->ev_fork, stream);
         if (e == hipSuccess) e = hipStreamWaitEvent(ms, f->ev_fork, 0);
     }
     if (e == hipSuccess)
         e = bk::run_plan(ms, f->side, f->plan[pi], W, m, n, mt, nt, f->ws, f->LA, f->LB, f->b_ident,
-                         qa, codes, V, pre, f->knear, f->items, tim, f->ev_rel.data(),
-                         f->ev_side.data());
+                         qa, codes, V, pre, f->knear, spin_limit, f->items, tim,
+                         f->ev_rel.data(), f->ev_side.data());
     if (fork && e == hipSuccess) {
         e = hipEventRecord(f->ev_join, ms);
         if (e == hipSuccess) e = hipStreamWaitEvent(stream, f->ev_join, 0);
@@ -902,7 +933,12 @@ extern "C" bakron_status bakron_solve_check(const bakron_factors* f, hipStream_t
     int32_t v = 0;
     hipError_t e = hipMemcpyAsync(&v, f->ws.status, sizeof(v), hipMemcpyDeviceToHost, stream);
     if (e == hipSuccess) e = hipStreamSynchronize(stream);
+    // the status is sticky: clear it once it has been reported
+    if (e == hipSuccess && v != 0) {
+        e = hipMemsetAsync(f->ws.status, 0, sizeof(int32_t), stream);
+        if (e == hipSuccess) e = hipStreamSynchronize(stream);
+    }
     if (e != hipSuccess) return hip_fail(&fm->err, e, "bakron_solve_check");
-    *failed = v;
+    *failed = v != 0;
     return BAKRON_OK;
 }

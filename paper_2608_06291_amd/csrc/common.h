@@ -79,14 +79,21 @@ struct Plan {
 };
 
 // Solve workspace: X, Y are mt*nt tile arrays of fp32; flags one int per
-// tile; counters one ticket counter per segment; status one int.
+// tile; counters one ticket counter per segment; status one int (set when a
+// wait gave up; cleared only by the host); scale_bad one int (debug scale
+// validation).  status and scale_bad are the last two words.
 struct Workspace {
     float* X;
     float* Y;
     int* flags;
     int* counters;
     int* status;
+    int* scale_bad;
 };
+
+// Polls of a tile ready flag before the wait gives up (never reached in a
+// correct run).
+constexpr int SPIN_LIMIT = 1 << 22;
 
 // Persistent segment launches use at most this many workgroups (one per CU).
 constexpr int SEG_GRID = 256;
@@ -136,6 +143,10 @@ __device__ inline float row_scale_of(const QuantArgs& q, int64_t row, const ColS
 
 // Fills n 32-bit words at p with v on stream st (debug poisoning).
 hipError_t fill_words(hipStream_t st, void* p, int64_t n, uint32_t v);
+
+// Sets *bad to 1 on stream st if any of `count` scales is negative, NaN or
+// infinite (*bad is not cleared here).
+hipError_t check_scales(hipStream_t st, const float* s, int64_t count, int* bad);
 
 // Records the message returned by bakron_last_error() for this thread.
 void set_last_error(const char* msg);

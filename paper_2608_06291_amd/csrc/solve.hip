@@ -58,21 +58,24 @@ struct SegArgs {
     int knear;        // pull distances 1..knear (<= KNEAR_MAX)
     int* flags;       // per tile: 1 once F of the tile is published
     int* counter;     // strip ticket counter of this launch, 0 at entry
-    int* status;      // set to 1 if a wait gave up (never in a correct run)
+    int* status;      // set to 1 if a wait gave up (never in a correct run); sticky
+    int spin_limit;   // polls before a wait gives up
 };
 
 // Bounded wait for a tile's ready flag, executed by a whole wave (uniform
 // address).  A strip only ever waits for strips with smaller tickets, and
 // tickets are handed out only to running workgroups, so the flag is set by a
 // running workgroup; the bound only turns a logic error into a reported
-// failure instead of a hang.  The data behind the flag is read with
+// failure instead of a hang.  Once a wait has given up, the status word stays
+// set (until the host reads and clears it) and every later wait returns at
+// once, so a failed solve, and every solve after it, ends quickly with its
+// output marked invalid.  The data behind the flag is read with
 // device-coherent (sc1) loads, so no cache invalidation is needed here.
-constexpr int SPIN_LIMIT = 1 << 22;
-__device__ inline void wait_ready(const int* flag, int* status) {
+__device__ inline void wait_ready(const int* flag, int* status, int spin_limit) {
     int it = 0;
     while (__hip_atomic_load(flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0) {
         __builtin_amdgcn_s_sleep(1);
-        if (++it >= SPIN_LIMIT ||
+        if (++it >= spin_limit ||
             __hip_atomic_load(status, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0) {
             __hip_atomic_store(status, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             break;
@@ -312,7 +315,7 @@ __global__ __launch_bounds__(512) void k_seg(SegArgs a) {
             // staged now.
             const bool lb_need = !a.b_ident && kc >= 1;
             if ((lb_need && !lb_staged) || (need_y && !y_staged) || I == I_first) {   // uniform
-                if (need_y && !y_staged) wait_ready(a.flags + I * a.nt + (J - 2), a.status);
+                if (need_y && !y_staged) wait_ready(a.flags + I * a.nt + (J - 2), a.status, a.spin_limit);
                 stage(I, lb_need && !lb_staged, need_y && !y_staged);
                 __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0): this wave's direct loads landed
                 __syncthreads();
@@ -322,7 +325,7 @@ __global__ __launch_bounds__(512) void k_seg(SegArgs a) {
                 for (; nk <= kmax; ++nk) pull_src(I, nk);
                 if (roww) {
                     if (kr >= 1) {   // distance 1: F[I, J-1] straight from memory after its flag
-                        wait_ready(a.flags + I * a.nt + (J - 1), a.status);
+                        wait_ready(a.flags + I * a.nt + (J - 1), a.status, a.spin_limit);
                         const __amdgpu_buffer_rsrc_t r1 = tile_rsrc(a.Y + ws_tile_offset(I, J - 1, a.nt));
                         const f32x4 b0 = __builtin_amdgcn_raw_buffer_load_b128(r1, (rb * TS + 8 * ks) * 4, 0, CPOL_SC1);
                         const f32x4 b1 = __builtin_amdgcn_raw_buffer_load_b128(r1, (rb * TS + 8 * ks + 4) * 4, 0, CPOL_SC1);
@@ -515,6 +518,25 @@ __global__ __launch_bounds__(256) void k_fill_u32(uint32_t* __restrict__ p, int6
         p[i] = v;
 }
 
+// *bad <- 1 if any of the `count` scales at s is negative, NaN or infinite
+// (the quantiser needs finite scales >= 0).  *bad is cleared by the caller.
+__global__ __launch_bounds__(256) void k_check_scales(const float* __restrict__ s, int64_t count,
+                                                       int* __restrict__ bad) {
+    bool ok = true;
+    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < count; i += (int64_t)gridDim.x * 256) {
+        const float v = s[i];
+        ok = ok && v >= 0.0f && v <= 3.402823466e38f;
+    }
+    if (!ok) __hip_atomic_store(bad, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+hipError_t check_scales(hipStream_t st, const float* s, int64_t count, int* bad) {
+    if (count <= 0) return hipSuccess;
+    const int64_t g = std::min<int64_t>((count + 255) / 256, 1024);
+    hipLaunchKernelGGL(k_check_scales, dim3((unsigned)g), dim3(256), 0, st, s, count, bad);
+    return hipGetLastError();
+}
+
 hipError_t fill_words(hipStream_t st, void* p, int64_t n, uint32_t v) {
     if (n <= 0) return hipSuccess;
     const int64_t g = std::min<int64_t>((n + 255) / 256, 65536);
@@ -680,15 +702,15 @@ __global__ __launch_bounds__(256, (MT == 4 ? 2 : 4)) void k_node(NodeArgs a) {
 }
 
 // X <- W (tile-major, column-major inside each tile, zero padding), Y <- 0,
-// ready flags <- 0 and ticket counters <- 0.  One workgroup per tile; the
+// ready flags <- 0 and ticket counters <- 0 (the give-up status word is left
+// as it is: it is cleared only when the host reads it).  One workgroup per tile; the
 // transpose goes through LDS so that both the read of W and the write of X
 // are coalesced.
 template <bool VEC>
 __global__ __launch_bounds__(256) void k_prep(const float* __restrict__ W, int64_t m, int64_t n,
                                               int mt, int nt, float* __restrict__ X,
                                               float* __restrict__ Y, int* __restrict__ flags,
-                                              int* __restrict__ counters, int ncounters,
-                                              int* __restrict__ status) {
+                                              int* __restrict__ counters, int ncounters) {
     __shared__ float T[TS][TS + 1];
     const int64_t tile = blockIdx.x;
     const int64_t I = tile / nt, J = tile - (tile / nt) * nt;
@@ -728,10 +750,8 @@ __global__ __launch_bounds__(256) void k_prep(const float* __restrict__ W, int64
         }
     }
     if (tid == 0) flags[tile] = 0;
-    if (tile == 0) {
+    if (tile == 0)
         for (int i = tid; i < ncounters; i += 256) counters[i] = 0;
-        if (tid == 0) *status = 0;
-    }
 }
 
 // ---------------------------------------------------------------------------
@@ -744,8 +764,8 @@ __global__ __launch_bounds__(256) void k_prep(const float* __restrict__ W, int64
 hipError_t run_plan(hipStream_t st, hipStream_t side, const Plan& plan, const float* W, int64_t m,
                     int64_t n, int mt, int nt, const Workspace& ws, const float* LA, const float* LB,
                     int b_ident, const QuantArgs& q, int8_t* codes, float* V, float* pre,
-                    int knear, const int4* items, hipEvent_t* tim, hipEvent_t* ev_rel,
-                    hipEvent_t* ev_side) {
+                    int knear, int spin_limit, const int4* items, hipEvent_t* tim,
+                    hipEvent_t* ev_rel, hipEvent_t* ev_side) {
     int ti = 0;
     auto t_begin = [&](hipStream_t s) { if (tim) (void)hipEventRecord(tim[2 * ti], s); };
     auto t_end = [&](hipStream_t s) { if (tim) (void)hipEventRecord(tim[2 * ti + 1], s); ++ti; };
@@ -753,10 +773,10 @@ hipError_t run_plan(hipStream_t st, hipStream_t side, const Plan& plan, const fl
     t_begin(st);
     if (n % 4 == 0 && reinterpret_cast<uintptr_t>(W) % 16 == 0)
         hipLaunchKernelGGL(k_prep<true>, dim3((unsigned)((int64_t)mt * nt)), dim3(256), 0, st, W, m,
-                           n, mt, nt, ws.X, ws.Y, ws.flags, ws.counters, plan.nseg, ws.status);
+                           n, mt, nt, ws.X, ws.Y, ws.flags, ws.counters, plan.nseg);
     else
         hipLaunchKernelGGL(k_prep<false>, dim3((unsigned)((int64_t)mt * nt)), dim3(256), 0, st, W, m,
-                           n, mt, nt, ws.X, ws.Y, ws.flags, ws.counters, plan.nseg, ws.status);
+                           n, mt, nt, ws.X, ws.Y, ws.flags, ws.counters, plan.nseg);
     t_end(st);
     if ((e = hipGetLastError()) != hipSuccess) return e;
 
@@ -765,6 +785,7 @@ hipError_t run_plan(hipStream_t st, hipStream_t side, const Plan& plan, const fl
     sa.LA = LA; sa.LB = LB; sa.b_ident = b_ident; sa.q = q;
     sa.codes = codes; sa.V = V; sa.pre = pre; sa.knear = knear; sa.flags = ws.flags;
     sa.status = ws.status;
+    sa.spin_limit = spin_limit;
     NodeArgs nd{};
     nd.knear = knear; nd.mt = mt; nd.nt = nt; nd.X = ws.X; nd.Y = ws.Y; nd.LA = LA; nd.LB = LB;
     auto node = [&](const PlanOp& op, hipStream_t s) {
