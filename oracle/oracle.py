@@ -13,6 +13,14 @@ Contents, each following a passage of arXiv 2608.06291:
   explicit inverse, then Cholesky (LAPACK via numpy, fp64).
 * :func:`babai` -- the sequential rounding itself: Alg. 2 (BaKron-naive) in C
   (``babai.c``), optionally tie-forced.
+* :func:`babai_recursive` -- the same rounding sequence by Alg. 5
+  (BaKron-recursive, Sec. 3.4): split the larger dimension in half, solve
+  the first half, feed its errors to the second half in one product (fp64
+  BLAS-3), solve the second half; Alg. 2 on small blocks.  O(mn(m+n)) work,
+  so it reaches the full-size layers.
+* :func:`normalized_factor_rev` -- the same factor by the RevCholesky route
+  (Sec. 3.1 definition): L = R^-1 diag(R), for sizes where the explicit
+  inverse of the literal route is too slow; the two routes are pinned equal.
 * :func:`ar1_diffusion` -- exact O(mn) special case for AR(1) Toeplitz A, B.
 * :func:`rev_cholesky` / :func:`certificate` -- closed-form check of any
   candidate output: by Eq. (1) the final workspace is
@@ -69,6 +77,11 @@ def _load():
         lib.oracle_babai_naive.argtypes = [
             ctypes.c_int64, ctypes.c_int64, dp, dp, dp, dp, ctypes.c_int, ctypes.c_int,
             i8p, ctypes.c_double, i8p, dp, dp, i64p, i64p, ctypes.c_int64]
+        lib.oracle_babai_recursive.restype = ctypes.c_int
+        lib.oracle_babai_recursive.argtypes = [
+            ctypes.c_int64, ctypes.c_int64, dp, dp, dp, dp, ctypes.c_int, ctypes.c_int,
+            i8p, ctypes.c_double, i8p, dp, dp, i64p, i64p, ctypes.c_int64, ctypes.c_int64,
+            ctypes.c_void_p]
         lib.oracle_ar1_diffusion.restype = ctypes.c_int
         lib.oracle_ar1_diffusion.argtypes = [
             ctypes.c_int64, ctypes.c_int64, dp, ctypes.c_double, ctypes.c_double,
@@ -182,6 +195,85 @@ def babai(W, LA, LB, scale, bits: int, forced=None, tie_window: float = 0.0,
         raise MemoryError("oracle_babai_naive: allocation failed")
     return dict(codes=codes, V=V, pre=pre, n_excused=int(exc.value),
                 n_flip=int(flip.value))
+
+
+def blas_dgemm_pointer():
+    """Address of the fp64 BLAS dgemm (Fortran interface) that scipy exports
+    for compiled extensions; used by babai_recursive for its products."""
+    import scipy.linalg.cython_blas as cb
+    cap = cb.__pyx_capi__["dgemm"]
+    get_name = ctypes.pythonapi.PyCapsule_GetName
+    get_name.restype = ctypes.c_char_p
+    get_name.argtypes = [ctypes.py_object]
+    get_ptr = ctypes.pythonapi.PyCapsule_GetPointer
+    get_ptr.restype = ctypes.c_void_p
+    get_ptr.argtypes = [ctypes.py_object, ctypes.c_char_p]
+    return get_ptr(cap, get_name(cap))
+
+
+def blas_threads() -> int:
+    """Threads of the BLAS behind blas_dgemm_pointer (scipy's OpenBLAS)."""
+    try:
+        import threadpoolctl
+        for info in threadpoolctl.threadpool_info():
+            if info.get("user_api") == "blas" and "scipy.libs" in info.get("filepath", ""):
+                return int(info["num_threads"])
+        for info in threadpoolctl.threadpool_info():
+            if info.get("user_api") == "blas":
+                return int(info["num_threads"])
+    except Exception:
+        pass
+    return 1
+
+
+def babai_recursive(W, LA, LB, scale, bits: int, forced=None, tie_window: float = 0.0,
+                    alphabet: str = "sym", base: int = 8, blas_min: int = 32768,
+                    use_blas: bool = True):
+    """The rounding of :func:`babai` (same codes) by Alg. 5 in C: feedback
+    batched by divide and conquer, products through fp64 BLAS dgemm when
+    M*N*K >= blas_min (plain loops below, or everywhere if not use_blas),
+    Alg. 2 on blocks of at most base x base.  Returns the same dict."""
+    lib = _load()
+    W = np.ascontiguousarray(W, dtype=np.float64)
+    m, n = W.shape
+    LA = np.ascontiguousarray(LA, dtype=np.float64)
+    LB = np.ascontiguousarray(LB, dtype=np.float64)
+    s = entry_scales(scale, m, n)
+    qlo, qhi = alphabet_bounds(bits, alphabet)
+    assert LA.shape == (n, n) and LB.shape == (m, m)
+    codes = np.zeros((m, n), np.int8)
+    V = np.zeros((m, n), np.float64)
+    pre = np.zeros((m, n), np.float64)
+    exc = ctypes.c_int64(0)
+    flip = ctypes.c_int64(0)
+    fp = None
+    if forced is not None:
+        forced = np.ascontiguousarray(forced, dtype=np.int8)
+        assert forced.shape == (m, n)
+        fp = _i8ptr(forced)
+    gemm = blas_dgemm_pointer() if use_blas else None
+    rc = lib.oracle_babai_recursive(m, n, _dptr(W), _dptr(LA), _dptr(LB), _dptr(s), qlo, qhi, fp,
+                                    float(tie_window), _i8ptr(codes), _dptr(V), _dptr(pre),
+                                    ctypes.byref(exc), ctypes.byref(flip), int(base),
+                                    int(blas_min), gemm)
+    if rc != 0:
+        raise MemoryError("oracle_babai_recursive: allocation failed")
+    return dict(codes=codes, V=V, pre=pre, n_excused=int(exc.value), n_flip=int(flip.value))
+
+
+def normalized_factor_rev(X, lam: float) -> np.ndarray:
+    """The factor of :func:`normalized_factor` by the RevCholesky route:
+    R = RevCholesky(X_d) (lower, R^T R = X_d, Sec. 3.1), L = R^-1 diag(R).
+    Equal in exact arithmetic to normalised Cholesky(X_d^-1): X_d^-1 =
+    R^-1 R^-T with R^-1 lower, so R^-1 D^-1 (D = diag(R^-1) = diag(R)^-1) is
+    the Cholesky factor, and normalising its columns gives R^-1 diag(R)."""
+    from scipy.linalg import lapack
+    R = rev_cholesky(damp(X, lam))
+    Rinv, info = lapack.dtrtri(R, lower=1)
+    if info != 0:
+        raise np.linalg.LinAlgError(f"dtrtri info {info}")
+    Rinv = np.tril(Rinv)
+    return Rinv * np.diag(R)[None, :]
 
 
 def solve(W, A, B, damp_lambda: float, scale, bits: int, forced=None,
