@@ -49,39 +49,62 @@ def cpu_model() -> str:
     return platform.processor() or "unknown"
 
 
-def cpu_baseline(cfg_inputs, seconds: float) -> dict:
-    """Time the fp64 oracle (Alg. 2, single-threaded C) on the first entries of
-    the same layer and extrapolate by its exact multiply-add count."""
+def cpu_baseline(cfg_inputs, rows: int) -> dict:
+    """The fp64 oracle's Alg. 5 (BaKron-recursive: divide and conquer with
+    BLAS-3 feedback, on every BLAS thread of the host) timed free-running on
+    a bounded sample of the same workload: the layer made of the first `rows`
+    output rows (those rows of W, the leading rows x rows block of the
+    output-side Gram B, all of A), solved in full including its own
+    factorisation (timed separately).  The rate is counted TFLOP/s
+    (rows * n * (rows + n) / seconds); ms_per_layer scales it to the whole
+    layer by counted work."""
     import numpy as np
     import oracle
-    W = cfg_inputs["W"].astype(np.float64)
+    W = cfg_inputs["W"]
     m, n = W.shape
-    LA = oracle.normalized_factor(cfg_inputs["A"], cfg_inputs["damp"])
-    LB = oracle.normalized_factor(cfg_inputs["B"], cfg_inputs["damp"])
-    s = cfg_inputs["scale"]
-    bits = cfg_inputs["bits"]
+    k = min(int(rows), m)
+    Ws = np.ascontiguousarray(W[:k])
+    Bs = np.ascontiguousarray(cfg_inputs["B"][:k, :k])
+    ss = np.ascontiguousarray(cfg_inputs["scale"][:k])
     t0 = time.perf_counter()
-    oracle.babai(W, LA, LB, s, bits, max_entries=1)
-    t_setup = time.perf_counter() - t0
-    probe = 16
+    LA = oracle.normalized_factor_rev(cfg_inputs["A"], cfg_inputs["damp"])
+    LB = oracle.normalized_factor_rev(Bs, cfg_inputs["damp"])
+    t_fac = time.perf_counter() - t0
     t0 = time.perf_counter()
-    oracle.babai(W, LA, LB, s, bits, max_entries=probe)
-    t_probe = time.perf_counter() - t0
-    per = max((t_probe - t_setup) / (probe - 1), 1e-6)
-    k = int(max(probe, min(m * n, seconds / per)))
-    t0 = time.perf_counter()
-    oracle.babai(W, LA, LB, s, bits, max_entries=k)
-    t_k = time.perf_counter() - t0
-    macs_k = oracle.naive_macs(m, n, k) - oracle.naive_macs(m, n, 1)
-    rate = macs_k / max(t_k - t_setup, 1e-9)           # multiply-adds per second
-    t_full = oracle.naive_macs(m, n) / rate + t_setup
+    oracle.babai_recursive(Ws, LA, LB, ss, cfg_inputs["bits"])
+    t_solve = time.perf_counter() - t0
+    F_sample = float(k) * n * (k + n)
     F = float(m) * n * (m + n)
-    return dict(value=F / t_full / 1e12, unit="TFLOP/s", cores=1, kind="oracle",
-                sample=(f"first {k} of {m*n} entries (row-major) of the same {m}x{n} layer, "
-                        f"Alg. 2 in single-threaded C, {t_k:.1f} s measured; full layer "
-                        f"extrapolated by its exact multiply-add count"),
-                ms_per_layer=t_full * 1e3, sample_seconds=t_k, host_cpu=cpu_model(),
-                host_nproc=os.cpu_count())
+    rate = F_sample / t_solve
+    threads = oracle.blas_threads()
+    return dict(value=rate / 1e12, unit="TFLOP/s", cores=threads, kind="oracle",
+                sample=(f"the {k}x{n} layer formed by the first {k} output rows of the same "
+                        f"{m}x{n} workload (W rows, leading {k}x{k} block of B, all of A), solved "
+                        f"in full by the fp64 oracle's Alg. 5 (BLAS-3 feedback on {threads} BLAS "
+                        f"threads, leaf rounding single-threaded) in {t_solve:.1f} s; "
+                        f"ms_per_layer scales the counted rate to the whole layer"),
+                ms_per_layer=F / rate * 1e3, sample_seconds=t_solve, factor_seconds=t_fac,
+                sample_counted_flops=F_sample, host_cpu=cpu_model(), host_nproc=os.cpu_count())
+
+
+def cpu_full(cfg_inputs) -> dict:
+    """The oracle's Alg. 5 on the whole layer, free-running, no extrapolation
+    (factorisation by the RevCholesky route timed separately)."""
+    import oracle
+    W = cfg_inputs["W"]
+    m, n = W.shape
+    t0 = time.perf_counter()
+    LA = oracle.normalized_factor_rev(cfg_inputs["A"], cfg_inputs["damp"])
+    LB = oracle.normalized_factor_rev(cfg_inputs["B"], cfg_inputs["damp"])
+    t_fac = time.perf_counter() - t0
+    log(f"[bench] cpu full: factors {t_fac:.1f} s")
+    t0 = time.perf_counter()
+    oracle.babai_recursive(W, LA, LB, cfg_inputs["scale"], cfg_inputs["bits"])
+    t_solve = time.perf_counter() - t0
+    F = float(m) * n * (m + n)
+    return dict(kind="oracle-full-layer", solve_seconds=t_solve, factor_seconds=t_fac,
+                counted_tflops=F / t_solve / 1e12, blas_threads=oracle.blas_threads(),
+                host_cpu=cpu_model(), host_nproc=os.cpu_count(), m=m, n=n)
 
 
 def validate_outputs(pk, f, W, s, bits, codes, V) -> dict:
@@ -99,7 +122,7 @@ def validate_outputs(pk, f, W, s, bits, codes, V) -> dict:
     l = (1 << (bits - 1)) - 1
     same = bool(torch.equal(cd, codes)) and bool(torch.equal(vd.view(torch.int32), V.view(torch.int32)))
     sv = (s[:, None] * codes.to(torch.float32))
-    v_ok = bool(torch.equal(sv.view(torch.int32), V.view(torch.int32)))
+    v_ok = bool(torch.equal(sv, V))     # value equality: V may hold -0.0 where x < 0 rounds to 0
     zero = (s == 0)[:, None].expand_as(x)
     q = torch.where(zero, torch.zeros_like(x), torch.clamp(torch.round(x), -l, l))
     own = bool(torch.equal(q.to(torch.int8), codes))
@@ -583,7 +606,13 @@ def main():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--profile-steps", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--cpu-seconds", type=float, default=15.0,
+                    help="with --factors: seconds of oracle work for its CPU baseline")
+    ap.add_argument("--cpu-rows", type=int, default=8192,
+                    help="rows of the layer sample the CPU baseline solves (oracle, Alg. 5)")
+    ap.add_argument("--cpu-full", action="store_true",
+                    help="only time the fp64 oracle (Alg. 5) on the whole configured layer on the "
+                         "host cores (no GPU work) and exit")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="only run a plain device-to-device copy of this many MiB (10 times) and "
                          "exit: the reference for scaling rocprofv3 FETCH_SIZE/WRITE_SIZE counters")
@@ -651,6 +680,14 @@ def main():
 
     import paper_2608_06291_amd as pk
     import workloads
+
+    if args.cpu_full:
+        log(f"[bench] generating config {args.config} (seed {args.seed})")
+        c = workloads.make(args.config, seed=args.seed, device="cuda")
+        out = cpu_full(c)
+        out["workload"] = c["cfg"].name
+        print(json.dumps(out), flush=True)
+        return
 
     dev = torch.device("cuda:0")
     log(f"[bench] generating config {args.config} (seed {args.seed})")
@@ -762,9 +799,11 @@ def main():
 
     cpu = None
     if not args.no_cpu_baseline:
-        log(f"[bench] cpu baseline (~{args.cpu_seconds:.0f} s of oracle work)")
-        cpu = cpu_baseline(c, args.cpu_seconds)
-        log(f"[bench] cpu baseline {cpu['ms_per_layer']:.0f} ms/layer (extrapolated)")
+        log(f"[bench] cpu baseline: oracle Alg. 5 on a {args.cpu_rows}-row sample")
+        cpu = cpu_baseline(c, args.cpu_rows)
+        log(f"[bench] cpu baseline {cpu['value'] * 1e3:.2f} counted GFLOP/s in "
+            f"{cpu['sample_seconds']:.1f} s ({cpu['cores']} BLAS threads); "
+            f"{cpu['ms_per_layer']:.0f} ms/layer by counted work")
 
     vs = None
     if (m, n) == (4096, 4096):

@@ -277,14 +277,16 @@ def normalized_factor_rev(X, lam: float) -> np.ndarray:
 
 
 def solve(W, A, B, damp_lambda: float, scale, bits: int, forced=None,
-          tie_window: float = 0.0, alphabet: str = "sym"):
-    """Factors by the literal route, then :func:`babai`.  B=None means I_m."""
+          tie_window: float = 0.0, alphabet: str = "sym", method: str = "naive"):
+    """Factors by the literal route, then :func:`babai` (method "naive",
+    Alg. 2) or :func:`babai_recursive` (method "recursive", Alg. 5; the
+    same codes).  B=None means I_m."""
     W = np.asarray(W, dtype=np.float64)
     m, n = W.shape
     LA = normalized_factor(A, damp_lambda)
     LB = np.eye(m) if B is None else normalized_factor(B, damp_lambda)
-    return babai(W, LA, LB, scale, bits, forced=forced, tie_window=tie_window,
-                 alphabet=alphabet)
+    run = {"naive": babai, "recursive": babai_recursive}[method]
+    return run(W, LA, LB, scale, bits, forced=forced, tie_window=tie_window, alphabet=alphabet)
 
 
 def naive_macs(m: int, n: int, entries: int | None = None) -> float:
@@ -381,6 +383,52 @@ def certificate(W, A, B, damp_lambda: float, scale, codes, bits: int,
         x = Wt / Sr
     x[Sr == 0.0] = np.nan
     return x
+
+
+def certify(W, A, B, damp_lambda: float, scale, codes, bits: int, window: float = 1e-4,
+            alphabet: str = "sym", row_block: int = 4096):
+    """Certificate, verdict and objective of a candidate output in one pass,
+    for every entry of a full-size layer (fp64, BLAS-3 triangular products).
+
+    With R_X = RevCholesky(X_d) (lower, R_X^T R_X = X_d), D = V - W0 and
+    T = R_B D R_A^T:
+      * pre-rounding values (closed form of Eq. (1), as :func:`certificate`):
+        W~ = V - diag(R_B)^-1 T diag(R_A)^-1, x = W~ / s;
+      * objective (Prop. 3.1): tr(D^T B_d D A_d) = |R_B D R_A^T|_F^2 = |T|_F^2.
+    Returns dict(verdict of :func:`verdict`, objective, x (m x n fp64)).
+    B = None means B = I.  Rows of T are formed in blocks of row_block."""
+    from scipy.linalg import blas
+    W = np.asarray(W, dtype=np.float64)
+    m, n = W.shape
+    S = entry_scales(scale, m, n)
+    V = S * np.asarray(codes, dtype=np.float64)
+    RA = rev_cholesky(damp(A, damp_lambda))
+    dA = np.diag(RA).copy()
+    D = V - W
+    # U = D R_A^T (right triangular product), column-major for BLAS
+    U = blas.dtrmm(1.0, np.asfortranarray(RA), np.asfortranarray(D), side=1, lower=1, trans_a=1)
+    del D
+    if B is None:
+        T = np.ascontiguousarray(U)
+        dB = np.ones(m)
+    else:
+        RB = rev_cholesky(damp(B, damp_lambda))
+        dB = np.diag(RB).copy()
+        T = np.empty((m, n), np.float64)
+        # T[rows] = R_B[rows, :r1] U[:r1]: R_B lower, so row block [r0, r1)
+        # needs only the first r1 rows of U
+        for r0 in range(0, m, row_block):
+            r1 = min(m, r0 + row_block)
+            T[r0:r1] = RB[r0:r1, :r1] @ U[:r1]
+        del RB
+    del U
+    obj = float(np.sum(T * T))
+    Wt = V - T / dB[:, None] / dA[None, :]
+    del T
+    with np.errstate(divide="ignore", invalid="ignore"):
+        x = Wt / S
+    x[S == 0.0] = np.nan
+    return dict(verdict=verdict(codes, x, bits, window, alphabet), objective=obj, x=x)
 
 
 def verdict(codes, x, bits: int, window: float = 1e-4, alphabet: str = "sym"):

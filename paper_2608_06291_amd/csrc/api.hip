@@ -49,6 +49,8 @@ struct bakron_factors {
     void* ws_mem = nullptr;         // X, Y tile arrays, flags, counters, status (bk::Workspace)
     bk::Workspace ws{};
     int knear = 8;
+    // node macro tile: 0 per node (default), 4 or 2 forced (BAKRON_MACRO)
+    int macro = 0;
     // BAKRON_POISON=1 at creation: fill the workspace with NaN / -1 before
     // every solve (debug aid: the solve must never read a word it did not
     // write first)
@@ -188,13 +190,15 @@ static void leaves(int K, int L, int knear, std::vector<std::pair<int, int>>& ou
     leaves(Mid, L, knear, out);
 }
 
+// macro: 0 chooses the macro tile per node (128 x 128 when a node has at
+// least 512 such items, else 64 x 64); 4 or 2 forces one size
 static bool node_op(int K, int Mid, int tlo, int thi, int mt, int nt, int knear, int b_ident,
-                    std::vector<int4>& items, bk::PlanOp& op) {
+                    std::vector<int4>& items, bk::PlanOp& op, int macro) {
     const double T = bk::TS;
-    int MT = bk::MACRO;
+    int MT = macro == 2 ? 2 : bk::MACRO;
     std::vector<int4> its;
-    node_items(K, Mid, tlo, thi, mt, nt, knear, b_ident, 4, its);
-    if ((int)its.size() < 512) {
+    node_items(K, Mid, tlo, thi, mt, nt, knear, b_ident, MT, its);
+    if (macro == 0 && (int)its.size() < 512) {
         MT = 2;
         node_items(K, Mid, tlo, thi, mt, nt, knear, b_ident, 2, its);
     }
@@ -218,7 +222,7 @@ static bool node_op(int K, int Mid, int tlo, int thi, int mt, int nt, int knear,
 }
 
 static void build_ops(int K, int L, int mt, int nt, int knear, int b_ident, bool defer,
-                      bk::Plan& plan, std::vector<int4>& items) {
+                      bk::Plan& plan, std::vector<int4>& items, int macro) {
     const double T = bk::TS, pair = 2.0 * T * T * T;
     if (L - K <= knear + 1) {
         bk::PlanOp op{};
@@ -247,7 +251,7 @@ static void build_ops(int K, int L, int mt, int nt, int knear, int b_ident, bool
         return;
     }
     const int Mid = (K + L) / 2;
-    build_ops(K, Mid, mt, nt, knear, b_ident, defer, plan, items);
+    build_ops(K, Mid, mt, nt, knear, b_ident, defer, plan, items, macro);
     // With `defer`, the push into the first right segment is a main op and the
     // pushes into the later segments are side ops released after the left
     // subtree; every target tile receives one addition per node either way.
@@ -255,15 +259,16 @@ static void build_ops(int K, int L, int mt, int nt, int knear, int b_ident, bool
     std::vector<std::pair<int, int>> right;
     leaves(Mid, L, knear, right);
     bk::PlanOp op;
-    if (node_op(K, Mid, Mid, defer ? right[0].second : L, mt, nt, knear, b_ident, items, op))
+    if (node_op(K, Mid, Mid, defer ? right[0].second : L, mt, nt, knear, b_ident, items, op, macro))
         plan.ops.push_back(op);
     if (defer)
         for (size_t j = 1; j < right.size(); ++j)
-            if (node_op(K, Mid, right[j].first, right[j].second, mt, nt, knear, b_ident, items, op)) {
+            if (node_op(K, Mid, right[j].first, right[j].second, mt, nt, knear, b_ident, items, op,
+                        macro)) {
                 op.rel = rel;
                 plan.side.push_back(op);
             }
-    build_ops(Mid, L, mt, nt, knear, b_ident, defer, plan, items);
+    build_ops(Mid, L, mt, nt, knear, b_ident, defer, plan, items, macro);
 }
 
 // side ops in deadline order (target segment, then release); per main op the
@@ -289,12 +294,12 @@ static void finish_plan(bk::Plan& plan) {
 }
 
 static void build_plan(int mt, int nt, int knear, int b_ident, bool defer, bk::Plan& plan,
-                       std::vector<int4>& items) {
+                       std::vector<int4>& items, int macro = 0) {
     plan.ops.clear();
     plan.side.clear();
     plan.nseg = 0;
     items.clear();
-    build_ops(0, mt + nt - 1, mt, nt, knear, b_ident, defer, plan, items);
+    build_ops(0, mt + nt - 1, mt, nt, knear, b_ident, defer, plan, items, macro);
     finish_plan(plan);
 }
 
@@ -320,6 +325,10 @@ extern "C" bakron_status bakron_factor(const float* A, int64_t n, const float* B
     if (const char* kn = std::getenv("BAKRON_KNEAR")) {
         int v = std::atoi(kn);
         if (v >= 0 && v <= bk::KNEAR_MAX) f->knear = v;
+    }
+    if (const char* mc = std::getenv("BAKRON_MACRO")) {
+        int v = std::atoi(mc);
+        if (v == 2 || v == 4) f->macro = v;
     }
 
     // A and B are factored concurrently (their block steps are latency-bound):
@@ -469,7 +478,7 @@ struct PlanEntry {
     hipStream_t main = nullptr, side = nullptr;
 };
 static std::mutex g_plan_mu;
-static std::map<std::tuple<int, int, int, int, int, int>, std::shared_ptr<PlanEntry>> g_plans;
+static std::map<std::tuple<int, int, int, int, int, int, int>, std::shared_ptr<PlanEntry>> g_plans;
 static std::map<std::pair<int, int>, std::pair<hipStream_t, hipStream_t>> g_streams;
 static std::set<int> g_streams_tried;   // devices whose default stream pair was requested
 
@@ -567,7 +576,7 @@ static double plan_model_seconds(const bk::Plan& p, int cus_main, int cus_side) 
 static bakron_status build_plan_entry(bakron_factors* f, int mt, int nt, int defer,
                                       PlanEntry& pe) {
     std::vector<int4> items_host;
-    build_plan(mt, nt, f->knear, f->b_ident, false, pe.plan[0], items_host);
+    build_plan(mt, nt, f->knear, f->b_ident, false, pe.plan[0], items_host, f->macro);
     pe.plan[1] = bk::Plan{};
     int ncu = 0;
     hipDeviceProp_t prop;
@@ -579,7 +588,7 @@ static bakron_status build_plan_entry(bakron_factors* f, int mt, int nt, int def
     if (ncu > 0 && ncu - R >= 64) {
         bk::Plan deferred;
         std::vector<int4> items;
-        build_plan(mt, nt, f->knear, f->b_ident, true, deferred, items);
+        build_plan(mt, nt, f->knear, f->b_ident, true, deferred, items, f->macro);
         deferred.side_cu_lo = R;
         // the overlap pays only while the pushes into later segments fit on
         // the side CUs during the chain; with more push work (tall or wide
@@ -612,7 +621,7 @@ static bakron_status build_plan_entry(bakron_factors* f, int mt, int nt, int def
 static bakron_status plan_with_side_stream(bakron_factors* f, int mt, int nt) {
     const char* env = std::getenv("BAKRON_DEFER");
     const int defer = env ? (std::atoi(env) == 0 ? 0 : 1) : 2;
-    const auto key = std::make_tuple(f->device, mt, nt, f->knear, f->b_ident, defer);
+    const auto key = std::make_tuple(f->device, mt, nt, f->knear, f->b_ident, defer, f->macro);
     std::shared_ptr<PlanEntry> pe;
     {
         std::lock_guard<std::mutex> lock(g_plan_mu);

@@ -103,8 +103,10 @@ def v_is_scale_times_code(V, codes, scale):
     return np.array_equal(V.view(np.uint32), ref.view(np.uint32)) or np.array_equal(V, ref)
 
 
-def check_against_oracle(p, codes, V, pre, oracle, label=""):
-    """Full element-by-element comparison with the tie-forced oracle replay."""
+def check_against_oracle(p, codes, V, pre, oracle, label="", method="naive"):
+    """Full element-by-element comparison with the tie-forced oracle replay
+    (method "naive": Alg. 2; "recursive": Alg. 5, the same sequence, for
+    shapes where the quartic Alg. 2 is slow)."""
     m, n = p["W"].shape
     assert codes.dtype == np.int8 and codes.shape == (m, n)
     alphabet = p.get("alphabet", "sym")
@@ -117,7 +119,7 @@ def check_against_oracle(p, codes, V, pre, oracle, label=""):
     if p.get("B_blocks") is not None:
         B = block_diag(p["B_blocks"])
     forced = oracle.solve(p["W"], p["A"], B, p["damp"], S, p["bits"],
-                          forced=codes, tie_window=TIE_WINDOW, alphabet=alphabet)
+                          forced=codes, tie_window=TIE_WINDOW, alphabet=alphabet, method=method)
     viol = int(np.count_nonzero(forced["codes"] != codes))
     flips = forced["n_flip"]
     res = dict(violations=viol, flips=flips, excused=forced["n_excused"], total=m * n)
@@ -140,7 +142,8 @@ def check_against_oracle(p, codes, V, pre, oracle, label=""):
     assert res["obj_rel"] <= OBJ_RTOL, f"{label}: objective rel diff {res['obj_rel']}"
     if flips == 0:
         # forcing changed nothing, so the free-running oracle must agree exactly
-        free = oracle.solve(p["W"], p["A"], B, p["damp"], S, p["bits"], alphabet=alphabet)
+        free = oracle.solve(p["W"], p["A"], B, p["damp"], S, p["bits"], alphabet=alphabet,
+                            method=method)
         assert np.array_equal(free["codes"], codes), f"{label}: free-running mismatch"
     return res
 

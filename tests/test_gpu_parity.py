@@ -154,3 +154,28 @@ def test_poisoned_workspace_bitwise(m, n, k, identity_B):
     ref_ad = gpu_run_antidiag(p)
     assert np.array_equal(ad[0], ref_ad[0]) and np.array_equal(ad[1].view(np.uint32),
                                                                ref_ad[1].view(np.uint32))
+
+
+@pytest.mark.parametrize("macro,k", [(4, 8), (4, 0), (2, 8)])
+def test_parity_forced_macro_tile(oracle_mod, macro, k):
+    """BAKRON_MACRO=4 makes every node push use the 128 x 128 macro tiles
+    (otherwise chosen only for nodes with >= 512 items, i.e. at full size),
+    =2 the 64 x 64 ones, on a shape whose tile counts (32 x 34) are not
+    multiples of 4, so the partial macro tiles and their masks run; every
+    entry against the oracle's tie-forced replay (Alg. 5, the same sequence
+    as Alg. 2)."""
+    import os
+    m, n = 1000, 1060
+    p = _problem(m, n, seed=4000 + macro + k)
+    log(f"case forced macro tile {macro} knear={k} m={m} n={n}")
+    old = os.environ.get("BAKRON_MACRO")
+    os.environ["BAKRON_MACRO"] = str(macro)
+    try:
+        codes, V, pre = gpu_run(p, k=k)
+    finally:
+        if old is None:
+            del os.environ["BAKRON_MACRO"]
+        else:
+            os.environ["BAKRON_MACRO"] = old
+    check_against_oracle(p, codes, V, pre, oracle_mod, label=f"macro{macro}-k{k}",
+                         method="recursive")

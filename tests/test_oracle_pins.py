@@ -331,3 +331,25 @@ def test_babai_beats_round_to_nearest(oracle_mod):
     Vr = c["scale"][:, None].astype(np.float64) * rtn
     assert o.objective(c["W"], r["V"], c["A"], c["B"], c["damp"]) < \
         o.objective(c["W"], Vr, c["A"], c["B"], c["damp"])
+
+
+@pytest.mark.parametrize("m,n,identity_B", [(40, 30, False), (30, 45, False), (25, 33, True)])
+def test_certify_matches_certificate_and_objective(oracle_mod, m, n, identity_B):
+    """The one-pass full-size certify() (triangular products, objective as
+    |R_B D R_A^T|_F^2) agrees with certificate() + verdict() and with the
+    explicit objective tr(D^T B_d D A_d); a planted wrong code is caught."""
+    o = oracle_mod
+    p = _rand_problem(m, n, seed=m + n, identity_B=identity_B)
+    r = o.solve(p["W"], p["A"], p["B"], p["damp"], p["scale"], p["bits"])
+    c = o.certify(p["W"], p["A"], p["B"], p["damp"], p["scale"], r["codes"], p["bits"],
+                  row_block=7)
+    x = o.certificate(p["W"], p["A"], p["B"], p["damp"], p["scale"], r["codes"], p["bits"])
+    np.testing.assert_allclose(c["x"], x, rtol=0, atol=1e-10)
+    np.testing.assert_allclose(c["x"], r["pre"], rtol=0, atol=1e-9)
+    assert c["verdict"]["violations"] == 0 and c["verdict"]["flips"] == 0
+    obj = o.objective(p["W"], r["V"], p["A"], p["B"], p["damp"])
+    assert abs(c["objective"] - obj) <= 1e-12 * obj
+    bad = r["codes"].copy()
+    bad[m // 2, n // 3] += 1 if bad[m // 2, n // 3] < 7 else -1
+    cb = o.certify(p["W"], p["A"], p["B"], p["damp"], p["scale"], bad, p["bits"])
+    assert cb["verdict"]["violations"] >= 1
