@@ -288,6 +288,35 @@ bakron_status bakron_profile_read(const bakron_factors *f, bakron_kernel_stat *s
  */
 bakron_status bakron_solve_check(const bakron_factors *f, hipStream_t stream, int32_t *failed);
 
+/*
+ * bakron_solve_noalloc -- bakron_solve for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc).  Same arguments, results (bitwise), ordering on
+ * `stream` and errors as bakron_solve, except:
+ *   - the solve workspace (two fp32 tile arrays of 4 * 1024 * ceil(m/32) *
+ *     ceil(n/32) bytes each, one int per tile and per segment launch) and the
+ *     node work list live in a static device array of 136 MiB that the
+ *     library holds on every GPU it runs on until the process exits; a layer
+ *     whose workspace and work list do not fit (more than about 17000 32 x 32
+ *     tiles, e.g. beyond 4096 x 4096) gives BAKRON_EINVAL before any work is
+ *     enqueued;
+ *   - it never calls hipMalloc / hipFree or any allocating routine; the first
+ *     call for a shape builds its launch plan in host memory (cached), and
+ *     every call copies the plan's work list (host -> device, a few MB at
+ *     most) into the array on `stream`;
+ *   - everything runs on `stream` (the one-stream plan; no fork);
+ *   - the current device must be the handle's device (else BAKRON_EINVAL).
+ * Every call on a GPU uses that GPU's one array, which keeps the last call's
+ * contents: calls that overlap in time on one GPU (on different streams, or
+ * from different threads or handles) race and give wrong results; serialise
+ * them.  bakron_solve_check on a handle that ran this call also reports (and
+ * clears) a give-up recorded in the array's status word, which is shared by
+ * every handle on the GPU.
+ */
+bakron_status bakron_solve_noalloc(const float *W, int64_t m, int64_t n, const bakron_factors *f,
+                                   bakron_quantizer q, int8_t *codes, float *V,
+                                   hipStream_t stream);
+
 /* ------------------------------------------------------------------------
  * Kronecker-factor construction from calibration samples (Sec. 4, App. A).
  *

@@ -8,5 +8,5 @@ from ._lib import (BAKRON_EHIP, BAKRON_EINVAL, BAKRON_ENOMEM, BAKRON_ENOTSPD, BA
                    EXPORTED, LIB_PATH, BakronError, Factors, factor, factor_blockdiag, gram,
                    gram_workspace_bytes, mse_scales,
                    kron_factors, load, mlp_local_factors, quadform_weights, sample_weights, solve,
-                   solve_antidiag,
+                   solve_antidiag, solve_noalloc,
                    status_string)

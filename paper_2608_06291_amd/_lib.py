@@ -20,7 +20,7 @@ EXPORTED = ("bakron_factor", "bakron_solve", "bakron_solve_debug", "bakron_facto
             "bakron_solve_check", "bakron_solve_antidiag", "bakron_gram",
             "bakron_sample_weights", "bakron_kron_factors", "bakron_mlp_local_factors",
             "bakron_mse_scales", "bakron_factor_blockdiag", "bakron_quadform_weights",
-            "bakron_kron_factors_iter", "bakron_mlp_local_factors_iter")
+            "bakron_kron_factors_iter", "bakron_mlp_local_factors_iter", "bakron_solve_noalloc")
 
 ALPHABETS = {"sym": 0, "asym": 1}
 
@@ -84,6 +84,9 @@ def load(path: str = LIB_PATH):
     lib.bakron_solve_antidiag.restype = ctypes.c_int
     lib.bakron_solve_antidiag.argtypes = [vp, ctypes.c_int64, ctypes.c_int64, vp, _Quantizer, vp, vp,
                                           vp, vp]
+    lib.bakron_solve_noalloc.restype = ctypes.c_int
+    lib.bakron_solve_noalloc.argtypes = [vp, ctypes.c_int64, ctypes.c_int64, vp, _Quantizer, vp, vp,
+                                         vp]
     lib.bakron_solve_check.restype = ctypes.c_int
     lib.bakron_solve_check.argtypes = [vp, vp, ctypes.POINTER(ctypes.c_int32)]
     i64, szp = ctypes.c_int64, ctypes.POINTER(ctypes.c_size_t)
@@ -279,6 +282,31 @@ def solve(W, f: Factors, bits: int, scale, codes=None, V=None, pre=None, debug: 
     if st != BAKRON_OK:
         raise BakronError(st, f.error())
     return (codes, V, pre) if debug else (codes, V)
+
+
+def solve_noalloc(W, f: Factors, bits: int, scale, codes=None, V=None, alphabet: str = "sym",
+                  group_size: int = 0, col_scale=None):
+    """bakron_solve_noalloc on the current stream: the solve with its workspace
+    in the library's static per-device scratch (no device allocation).
+    Quantiser arguments as :func:`solve`; codes and V are allocated here by
+    torch only if not given.  Returns (codes int8, V fp32)."""
+    import torch
+    lib = load()
+    _check_dev(W, "W", torch.float32)
+    m, n = W.shape
+    q = _quantizer(bits, scale, m, n, alphabet, group_size, col_scale)
+    if codes is None:
+        codes = torch.empty((m, n), dtype=torch.int8, device=W.device)
+    if V is None:
+        V = torch.empty((m, n), dtype=torch.float32, device=W.device)
+    _check_dev(codes, "codes", torch.int8)
+    _check_dev(V, "V", torch.float32)
+    st = lib.bakron_solve_noalloc(ctypes.c_void_p(W.data_ptr()), m, n, f.handle, q,
+                                  ctypes.c_void_p(codes.data_ptr()), ctypes.c_void_p(V.data_ptr()),
+                                  _stream(torch, W.device))
+    if st != BAKRON_OK:
+        raise BakronError(st, f.error())
+    return codes, V
 
 
 def solve_antidiag(W, f: Factors, bits: int, scale, codes=None, V=None, pre=None,

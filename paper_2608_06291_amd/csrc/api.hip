@@ -75,6 +75,10 @@ struct bakron_factors {
     int side_cu_lo = -1;
     std::vector<hipEvent_t> ev_rel, ev_side;
     hipEvent_t ev_fork = nullptr, ev_join = nullptr;
+    // set once a bakron_solve_noalloc on this handle has used its device's
+    // static scratch (bakron_solve_check then reads that status word too)
+    int noalloc_used = 0;
+    int* noalloc_status = nullptr;   // give-up word of the last allocation-free solve
     // BaKron-antidiagonal working copy of W and one diagonal's errors
     int64_t ad_m = -1, ad_n = -1;
     float* ad_mem = nullptr;
@@ -933,21 +937,149 @@ extern "C" bakron_status bakron_profile_read(const bakron_factors* f, bakron_ker
     return BAKRON_OK;
 }
 
+// ---------------------------------------------------------------------------
+// Allocation-free solve.  The solve workspace (the X and Y tile arrays, the
+// tile ready flags, the ticket counters, the sticky give-up word) and the node
+// work list live in one static device array per GPU instead of a hipMalloc'd
+// buffer.  Its device address is taken once per device with
+// hipGetSymbolAddress (the array's name is only a host-side stand-in) and kept
+// in g_noalloc_ptr.  Plans are built on the host and cached per shape (host
+// memory only); the work list is copied into the array by every call.
+constexpr size_t NOALLOC_SCRATCH_BYTES = (size_t)136 << 20;
+static __device__ __align__(256) unsigned char scratch[NOALLOC_SCRATCH_BYTES];
+
+struct HostPlan {
+    bk::Plan plan;
+    std::vector<int4> items;
+};
+static std::mutex g_noalloc_mu;
+static std::map<int, unsigned char*> g_noalloc_ptr;   // device -> address of `scratch`
+static std::map<std::tuple<int, int, int, int, int>, std::shared_ptr<HostPlan>> g_host_plans;
+
+// Byte layout of the scratch array: the sticky give-up word and the scale
+// flag at offset 0 (the same place for every shape), then X, Y, the ready
+// flags and ticket counters, then the work list.
+struct NoallocLayout {
+    size_t x_off, fbytes, ints_off, items_off, total;
+};
+static NoallocLayout noalloc_layout(int64_t tiles, int nseg, size_t nitems) {
+    NoallocLayout L;
+    L.x_off = 256;
+    L.fbytes = sizeof(float) * (size_t)tiles * bk::TILE_ELEMS;
+    L.ints_off = L.x_off + 2 * L.fbytes;
+    const size_t ibytes = sizeof(int) * ((size_t)tiles + (size_t)nseg);
+    L.items_off = (L.ints_off + ibytes + 255) / 256 * 256;
+    L.total = L.items_off + sizeof(int4) * nitems;
+    return L;
+}
+
+extern "C" bakron_status bakron_solve_noalloc(const float* W, int64_t m, int64_t n,
+                                             const bakron_factors* fc, bakron_quantizer q,
+                                             int8_t* codes, float* V, hipStream_t stream) {
+    bakron_factors* f = const_cast<bakron_factors*>(fc);
+    if (!f) return BAKRON_EINVAL;
+    f->err.clear();
+    bakron_status st = check_solve_args(f, "bakron_solve_noalloc", W, m, n, q, codes, V);
+    if (st != BAKRON_OK) return st;
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(&f->err, e, "bakron_solve_noalloc: hipGetDevice");
+    if (dev != f->device) {
+        f->err = "bakron_solve_noalloc: the current device is not the handle's device";
+        return BAKRON_EINVAL;
+    }
+    const int mt = (int)cdiv(m, bk::TS), nt = (int)cdiv(n, bk::TS);
+    const int64_t tiles = (int64_t)mt * nt;
+    // the workspace alone must fit before any plan is built
+    if (256 + 2 * sizeof(float) * (size_t)tiles * bk::TILE_ELEMS > NOALLOC_SCRATCH_BYTES) {
+        f->err = "bakron_solve_noalloc: layer too large for the static scratch (at most 136 MiB: "
+                 "ceil(m/32) * ceil(n/32) <= 17000 tiles, e.g. 4096 x 4096)";
+        return BAKRON_EINVAL;
+    }
+    std::shared_ptr<HostPlan> hp;
+    unsigned char* base = nullptr;
+    bool first_on_device = false;
+    {
+        std::lock_guard<std::mutex> lock(g_noalloc_mu);
+        const auto key = std::make_tuple(mt, nt, f->knear, f->b_ident, f->macro);
+        auto it = g_host_plans.find(key);
+        if (it != g_host_plans.end()) {
+            hp = it->second;
+        } else {
+            hp = std::make_shared<HostPlan>();
+            build_plan(mt, nt, f->knear, f->b_ident, false, hp->plan, hp->items, f->macro);
+            g_host_plans[key] = hp;
+        }
+        auto pit = g_noalloc_ptr.find(dev);
+        if (pit != g_noalloc_ptr.end()) {
+            base = pit->second;
+        } else {
+            void* ptr = nullptr;
+            e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+            if (e != hipSuccess || !ptr)
+                return hip_fail(&f->err, e != hipSuccess ? e : hipErrorInvalidSymbol,
+                                "bakron_solve_noalloc: hipGetSymbolAddress(scratch)");
+            base = static_cast<unsigned char*>(ptr);
+            g_noalloc_ptr[dev] = base;
+            first_on_device = true;
+        }
+    }
+    const NoallocLayout L = noalloc_layout(tiles, hp->plan.nseg, hp->items.size());
+    if (L.total > NOALLOC_SCRATCH_BYTES) {
+        f->err = "bakron_solve_noalloc: workspace and work list exceed the 136 MiB static scratch";
+        return BAKRON_EINVAL;
+    }
+    int* ints = reinterpret_cast<int*>(base + L.ints_off);
+    int* st_words = reinterpret_cast<int*>(base);
+    bk::Workspace ws{reinterpret_cast<float*>(base + L.x_off),
+                     reinterpret_cast<float*>(base + L.x_off + L.fbytes), ints, ints + tiles,
+                     st_words, st_words + 1};
+    // the give-up word is sticky (cleared only by bakron_solve_check); it is
+    // cleared once when the device's array is first used, with a fill kernel
+    // (no memset node, so a caller may capture this call)
+    e = hipSuccess;
+    if (first_on_device) e = bk::fill_words(stream, st_words, 2, 0u);
+    const int4* items = reinterpret_cast<const int4*>(base + L.items_off);
+    if (e == hipSuccess && !hp->items.empty())
+        e = hipMemcpyAsync(base + L.items_off, hp->items.data(), sizeof(int4) * hp->items.size(),
+                           hipMemcpyHostToDevice, stream);
+    int spin_limit = bk::SPIN_LIMIT;
+    if (const char* sl = std::getenv("BAKRON_SPIN_LIMIT")) {
+        const int v = std::atoi(sl);
+        if (v >= 1 && v <= bk::SPIN_LIMIT) spin_limit = v;
+    }
+    if (e == hipSuccess)
+        e = bk::run_plan(stream, nullptr, hp->plan, W, m, n, mt, nt, ws, f->LA, f->LB, f->b_ident,
+                         quant_args(q, n), codes, V, nullptr, f->knear, spin_limit, items, nullptr,
+                         nullptr, nullptr);
+    if (e != hipSuccess) return hip_fail(&f->err, e, "bakron_solve_noalloc: launch");
+    f->noalloc_used = 1;
+    f->noalloc_status = st_words;
+    return BAKRON_OK;
+}
+
 extern "C" bakron_status bakron_solve_check(const bakron_factors* f, hipStream_t stream,
                                            int32_t* failed) {
     if (!f || !failed) return BAKRON_EINVAL;
     bakron_factors* fm = const_cast<bakron_factors*>(f);
     *failed = 0;
-    if (!f->ws_mem) return BAKRON_OK;
-    int32_t v = 0;
-    hipError_t e = hipMemcpyAsync(&v, f->ws.status, sizeof(v), hipMemcpyDeviceToHost, stream);
-    if (e == hipSuccess) e = hipStreamSynchronize(stream);
-    // the status is sticky: clear it once it has been reported
-    if (e == hipSuccess && v != 0) {
-        e = hipMemsetAsync(f->ws.status, 0, sizeof(int32_t), stream);
+    // the handle's own workspace, and the device's static scratch if an
+    // allocation-free solve on this handle used it
+    int* words[2] = {f->ws_mem ? f->ws.status : nullptr, f->noalloc_used ? f->noalloc_status : nullptr};
+    int32_t any = 0;
+    for (int* w : words) {
+        if (!w) continue;
+        int32_t v = 0;
+        hipError_t e = hipMemcpyAsync(&v, w, sizeof(v), hipMemcpyDeviceToHost, stream);
         if (e == hipSuccess) e = hipStreamSynchronize(stream);
+        // the status is sticky: clear it once it has been reported
+        if (e == hipSuccess && v != 0) {
+            e = hipMemsetAsync(w, 0, sizeof(int32_t), stream);
+            if (e == hipSuccess) e = hipStreamSynchronize(stream);
+        }
+        if (e != hipSuccess) return hip_fail(&fm->err, e, "bakron_solve_check");
+        any |= v != 0;
     }
-    if (e != hipSuccess) return hip_fail(&fm->err, e, "bakron_solve_check");
-    *failed = v != 0;
+    *failed = any;
     return BAKRON_OK;
 }
