@@ -594,23 +594,43 @@ __global__ __launch_bounds__(256, (MT == 4 ? 2 : 4)) void k_node(NodeArgs a) {
     const int lr = l & 31, lk = l >> 5;
     const int srow = tid >> 3, sk = (tid & 7) * 4;   // staging: one float4 of each tile
 
-    auto a_tile = [&](int t, int kt) -> const float* {
-        if (colpush) {
-            const int I = I0 + t;
-            return (I < a.mt && kt <= I - a.knear - 1) ? a.LB + packed_tile_offset(I, kt) : nullptr;
-        }
-        const int J = J0 + t;
-        return (J < a.nt && kt <= J - a.knear - 1) ? a.LA + packed_tile_offset(J, kt) : nullptr;
-    };
-    auto b_tile = [&](int t, int kt) -> const float* {
-        if (colpush) {
-            const int J = J0 + t;
-            return (J < a.nt && kt + J >= a.K && kt + J < a.Mid) ? a.X + ws_tile_offset(kt, J, a.nt)
-                                                                 : nullptr;
-        }
-        const int I = I0 + t;
-        return (I < a.mt && I + kt >= a.K && I + kt < a.Mid) ? a.Y + ws_tile_offset(I, kt, a.nt)
-                                                             : nullptr;
+    // Operand tile t of K chunk kt as a buffer resource: a valid tile covers
+    // its 4 KB, an invalid one (outside the matrix, outside the (source,
+    // target) masks or past the item's range) has no records, so its loads
+    // return zeros without touching memory.  Every chunk therefore issues the
+    // same loads unconditionally, which lets the compiler wait only for the
+    // chunk it stores (the two-ahead prefetch stays in flight).  Per operand
+    // tile the valid chunks form one range [lo, hi) and consecutive chunks sit
+    // a fixed stride apart, so the per-item set-up below leaves two compares
+    // and an address per tile per chunk.
+    //   column push: A = L^B[I0 + t, kt] (kt <= I - knear - 1), B = E[kt, J0 + t]
+    //                (kt + J in [K, Mid)), read from X;
+    //   row push:    A = L^A[J0 + t, kt] (kt <= J - knear - 1), B = F[I0 + t, kt]
+    //                (I + kt in [K, Mid)), read from Y.
+    const float* abase[MT];
+    const float* bbase[MT];
+    int alo[MT], ahi[MT], blo[MT], bhi[MT];
+    const int64_t bstride = colpush ? (int64_t)a.nt * TILE_ELEMS : TILE_ELEMS;
+#pragma unroll
+    for (int t = 0; t < MT; ++t) {
+        const int Ia = colpush ? I0 + t : J0 + t;   // factor tile row
+        const bool arow = colpush ? Ia < a.mt : Ia < a.nt;
+        abase[t] = arow ? (colpush ? a.LB : a.LA) + packed_tile_offset(Ia, 0) : a.LA;
+        alo[t] = 0;
+        ahi[t] = arow ? min(khi, Ia - a.knear) : 0;
+        const int Ib = colpush ? J0 + t : I0 + t;   // fixed coordinate of the source tile
+        const bool brow = colpush ? Ib < a.nt : Ib < a.mt;
+        bbase[t] = brow ? (colpush ? a.X + ws_tile_offset(0, Ib, a.nt) : a.Y + ws_tile_offset(Ib, 0, a.nt))
+                        : a.LA;
+        blo[t] = max(a.K - Ib, 0);
+        bhi[t] = brow ? min(khi, a.Mid - Ib) : 0;
+    }
+    // (an invalid tile's address may lie outside every allocation: with no
+    // records nothing is read)
+    auto rsrc = [](const float* base, int64_t stride, int kt, int lo, int hi) {
+        const int nrec = (kt >= lo && kt < hi) ? TILE_ELEMS * 4 : 0;
+        return __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(base + kt * stride), (short)0, nrec,
+                                                 0x00020000);
     };
     // two register sets: while chunk kt is multiplied from LDS, chunk kt + 1
     // (loaded one iteration earlier) waits in one set and chunk kt + 2 is in
@@ -620,10 +640,10 @@ __global__ __launch_bounds__(256, (MT == 4 ? 2 : 4)) void k_node(NodeArgs a) {
     auto load = [&](int kt, int r) {
 #pragma unroll
         for (int t = 0; t < MT; ++t) {
-            const float* pa = a_tile(t, kt);
-            const float* pb = b_tile(t, kt);
-            ra[r][t] = pa ? *reinterpret_cast<const f32x4*>(pa + tid * 4) : f32x4{0.f, 0.f, 0.f, 0.f};
-            rb[r][t] = pb ? *reinterpret_cast<const f32x4*>(pb + tid * 4) : f32x4{0.f, 0.f, 0.f, 0.f};
+            ra[r][t] = __builtin_amdgcn_raw_buffer_load_b128(
+                rsrc(abase[t], TILE_ELEMS, kt, alo[t], ahi[t]), tid * 16, 0, 0);
+            rb[r][t] = __builtin_amdgcn_raw_buffer_load_b128(
+                rsrc(bbase[t], bstride, kt, blo[t], bhi[t]), tid * 16, 0, 0);
         }
     };
     auto store = [&](int s, int r) {
@@ -643,7 +663,7 @@ __global__ __launch_bounds__(256, (MT == 4 ? 2 : 4)) void k_node(NodeArgs a) {
     // one K chunk: multiply LDS buffer s; issue the load of chunk kt + 2 into
     // register set r, then move chunk kt + 1 (set r ^ 1) into buffer s ^ 1
     auto chunk = [&](int kt, int s, int r) {
-        if (kt + 2 < khi) load(kt + 2, r);
+        load(kt + 2, r);   // past the range: no records, zeros
         f32x4 fa[WB][4], fb[WB][4];
 #pragma unroll
         for (int x = 0; x < WB; ++x)
@@ -672,7 +692,7 @@ __global__ __launch_bounds__(256, (MT == 4 ? 2 : 4)) void k_node(NodeArgs a) {
     };
 
     load(klo, 0);
-    if (klo + 1 < khi) load(klo + 1, 1);
+    load(klo + 1, 1);
     store(0, 0);
     __syncthreads();
     // chunk klo + 2i uses buffer 0 and register set 0 for its prefetch,
