@@ -150,8 +150,9 @@ def measured_traffic(kernel: str, workload: str, sources=("solve.hip", "common.h
 
 
 def table3(max_antidiag_elems: int):
-    """Runtime comparison on the paper's Table 3 shapes: GPTQ (B = I through
-    the same solver), BaKron and BaKron-antidiagonal (Alg. 3), solve only
+    """Runtime comparison on the paper's Table 3 shapes: GPTQ (B = I: the
+    one-sided kernel, Alg. 1 on every row), BaKron and BaKron-antidiagonal
+    (Alg. 3), solve only
     (factorisation excluded, as in the paper).  Synthetic inputs: A, B the
     AR(1) Toeplitz matrices rho^|i-j| (rho 0.5 / 0.2), W ~ N(0, 0.02^2), per-row
     INT4 scales max|W_i|/7, damping 0.01.  Prints one JSON line per shape."""

@@ -5,7 +5,7 @@ import subprocess
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 SOURCES = ["csrc/api.hip", "csrc/factor.hip", "csrc/solve.hip", "csrc/antidiag.hip",
-           "csrc/hessian.hip", "csrc/quant.hip"]
+           "csrc/hessian.hip", "csrc/quant.hip", "csrc/gptq.hip"]
 LIB = os.path.join(HERE, "libbakron.so")
 
 HIPCC_FLAGS = [

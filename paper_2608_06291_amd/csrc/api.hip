@@ -34,6 +34,9 @@ int plan_timed_launches(const Plan& plan);
 hipError_t run_antidiag(hipStream_t st, const float* W, int64_t m, int64_t n, float* Wt,
                         float* delta, const float* LA, const float* LB, const QuantArgs& q,
                         int8_t* codes, float* V, float* pre);
+size_t gptq_workspace_floats(int64_t m, int64_t n);
+hipError_t run_gptq(hipStream_t st, const float* W, int64_t m, int64_t n, const float* LA, float* E,
+                    const QuantArgs& q, int8_t* codes, float* V, float* pre);
 }  // namespace bk
 
 struct bakron_factors {
@@ -79,6 +82,12 @@ struct bakron_factors {
     // static scratch (bakron_solve_check then reads that status word too)
     int noalloc_used = 0;
     int* noalloc_status = nullptr;   // give-up word of the last allocation-free solve
+    // B = I: the one-sided (GPTQ) path and its error workspace (E rows, then
+    // one int for the debug scale check); BAKRON_GPTQ=0 at creation sends
+    // B = I solves through the two-sided solver instead
+    int gptq = 1;
+    int64_t gq_m = -1, gq_n = -1;
+    float* gq_mem = nullptr;
     // BaKron-antidiagonal working copy of W and one diagonal's errors
     int64_t ad_m = -1, ad_n = -1;
     float* ad_mem = nullptr;
@@ -330,6 +339,7 @@ extern "C" bakron_status bakron_factor(const float* A, int64_t n, const float* B
         int v = std::atoi(kn);
         if (v >= 0 && v <= bk::KNEAR_MAX) f->knear = v;
     }
+    if (const char* gq = std::getenv("BAKRON_GPTQ")) f->gptq = std::atoi(gq) != 0;
     if (const char* mc = std::getenv("BAKRON_MACRO")) {
         int v = std::atoi(mc);
         if (v == 2 || v == 4) f->macro = v;
@@ -442,6 +452,7 @@ extern "C" void bakron_factors_free(bakron_factors* f) {
     if (f->LB) hipFree(f->LB);
     if (f->ws_mem) hipFree(f->ws_mem);
     if (f->ad_mem) hipFree(f->ad_mem);
+    if (f->gq_mem) hipFree(f->gq_mem);
     // f->side, f->main and f->items belong to the process-wide plan cache
     if (f->ev_fork) hipEventDestroy(f->ev_fork);
     if (f->ev_join) hipEventDestroy(f->ev_join);
@@ -765,6 +776,53 @@ static bakron_status check_solve_args(bakron_factors* f, const char* who, const 
     return BAKRON_OK;
 }
 
+// debug mode: every scale must be finite and >= 0 (a device reduction into
+// the flag word `bad_dev`, then one synchronisation of `stream`)
+static bakron_status debug_scale_check(bakron_factors* f, const bakron_quantizer& q,
+                                       const bk::QuantArgs& qa, int64_t m, int64_t n, int* bad_dev,
+                                       hipStream_t stream) {
+    const int64_t ns = m * (int64_t)qa.ngroups;
+    int32_t bad = 0;
+    hipError_t ce = hipMemsetAsync(bad_dev, 0, sizeof(int), stream);
+    if (ce == hipSuccess) ce = bk::check_scales(stream, q.scale, ns, bad_dev);
+    if (ce == hipSuccess && q.col_scale) ce = bk::check_scales(stream, q.col_scale, n, bad_dev);
+    if (ce == hipSuccess) ce = hipMemcpyAsync(&bad, bad_dev, sizeof(bad), hipMemcpyDeviceToHost, stream);
+    if (ce == hipSuccess) ce = hipStreamSynchronize(stream);
+    if (ce != hipSuccess) return hip_fail(&f->err, ce, "bakron_solve_debug: scale check");
+    if (bad) {
+        f->err = "bakron_solve_debug: a scale is negative, NaN or infinite";
+        return BAKRON_EINVAL;
+    }
+    return BAKRON_OK;
+}
+
+// B = I: the rows are independent (GPTQ with Hessian A on every row); one launch
+static bakron_status solve_gptq(bakron_factors* f, const float* W, int64_t m, int64_t n,
+                                const bakron_quantizer& q, int8_t* codes, float* V, float* pre,
+                                hipStream_t stream) {
+    const size_t ef = bk::gptq_workspace_floats(m, n);
+    if (f->gq_m != m || f->gq_n != n || !f->gq_mem) {
+        if (f->gq_mem) { hipFree(f->gq_mem); f->gq_mem = nullptr; }
+        f->gq_m = f->gq_n = -1;
+        hipError_t e = hipMalloc(&f->gq_mem, sizeof(float) * ef + 256);
+        if (e != hipSuccess) return hip_fail(&f->err, e, "bakron_solve: hipMalloc (one-sided workspace)");
+        f->gq_m = m;
+        f->gq_n = n;
+    }
+    const bk::QuantArgs qa = quant_args(q, n);
+    int* bad_dev = reinterpret_cast<int*>(f->gq_mem + ef);
+    if (pre) {
+        bakron_status st = debug_scale_check(f, q, qa, m, n, bad_dev, stream);
+        if (st != BAKRON_OK) return st;
+    }
+    hipError_t e = hipSuccess;
+    if (f->poison) e = bk::fill_words(stream, f->gq_mem, (int64_t)ef, 0xFFFFFFFFu);
+    if (e == hipSuccess) e = bk::run_gptq(stream, W, m, n, f->LA, f->gq_mem, qa, codes, V, pre);
+    if (e != hipSuccess) return hip_fail(&f->err, e, "bakron_solve: launch (one-sided)");
+    f->prof_valid = 0;   // the per-launch measurement hook covers the two-sided solver only
+    return BAKRON_OK;
+}
+
 static bakron_status solve_impl(const float* W, int64_t m, int64_t n, const bakron_factors* fc,
                                 bakron_quantizer q, int8_t* codes, float* V, float* pre,
                                 hipStream_t stream) {
@@ -773,26 +831,14 @@ static bakron_status solve_impl(const float* W, int64_t m, int64_t n, const bakr
     f->err.clear();
     bakron_status st = check_solve_args(f, "bakron_solve", W, m, n, q, codes, V);
     if (st != BAKRON_OK) return st;
+    if (f->b_ident && f->gptq) return solve_gptq(f, W, m, n, q, codes, V, pre, stream);
     st = ensure_workspace(f, m, n);
     if (st != BAKRON_OK) return st;
     const int mt = (int)cdiv(m, bk::TS), nt = (int)cdiv(n, bk::TS);
     const bk::QuantArgs qa = quant_args(q, n);
     if (pre) {
-        // debug mode: every scale must be finite and >= 0 (a device reduction,
-        // then one synchronisation of `stream`)
-        const int64_t ns = m * (int64_t)qa.ngroups;
-        int32_t bad = 0;
-        hipError_t ce = hipMemsetAsync(f->ws.scale_bad, 0, sizeof(int), stream);
-        if (ce == hipSuccess) ce = bk::check_scales(stream, q.scale, ns, f->ws.scale_bad);
-        if (ce == hipSuccess && q.col_scale) ce = bk::check_scales(stream, q.col_scale, n, f->ws.scale_bad);
-        if (ce == hipSuccess)
-            ce = hipMemcpyAsync(&bad, f->ws.scale_bad, sizeof(bad), hipMemcpyDeviceToHost, stream);
-        if (ce == hipSuccess) ce = hipStreamSynchronize(stream);
-        if (ce != hipSuccess) return hip_fail(&f->err, ce, "bakron_solve_debug: scale check");
-        if (bad) {
-            f->err = "bakron_solve_debug: a scale is negative, NaN or infinite";
-            return BAKRON_EINVAL;
-        }
+        st = debug_scale_check(f, q, qa, m, n, f->ws.scale_bad, stream);
+        if (st != BAKRON_OK) return st;
     }
     // polls before a tile-ordering wait gives up; BAKRON_SPIN_LIMIT (read at
     // every solve) lowers it, to exercise the give-up path from the host

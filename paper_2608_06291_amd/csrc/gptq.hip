@@ -1,0 +1,181 @@
+// One-sided rounding for B = I (GPTQ, Alg. 1 applied to every row of W with
+// the Hessian A; Sec. 1 and Table 1: n sequential steps, O(mn^2) work).
+//
+// With B = I the feedback of Eq. (1) never crosses rows:
+//     W~_pq = W0_pq + sum_{j<q} E_pj L^A_qj ,   E = V - W~ ,
+// so the rows are independent and each row is a sequential pass over its n
+// columns.  The columns are taken in blocks of 32 (one factor tile):
+//   1. lazy feedback: W~[rows, blk] = W0[rows, blk] + E[rows, 0:32b] L^A[blk, 0:32b]^T,
+//      a dense product on fp32 MFMA (the errors of all earlier blocks, kept
+//      in a row-major workspace);
+//   2. the 32 columns of the block in order: quantise column j of every row,
+//      then add E[:, j] L^A[q, j] to the later columns q of the block.
+// This is GPTQ's lazy batch update (the blocked form of Alg. 1); the sums are
+// the same elementary updates of Eq. (1), in another order.
+//
+// A workgroup owns 16 rows and walks all column blocks.  In step 1 each of
+// its 4 waves multiplies a quarter of the source tiles (tile kt = w, w + 4,
+// ...) with v_mfma_f32_16x16x4f32 (A = the 16 error rows, B = the factor tile
+// rows, so D[i][j] = sum_k E[i][k] L^A[j][k]); the four partial sums meet in
+// LDS.  In step 2 each wave owns 4 rows, 16 lanes per row with the block
+// columns c and c + 16 in registers; the error of column j is broadcast along
+// its 16 lanes with a lane shuffle, so no barrier is needed inside the block.
+#include "common.h"
+
+namespace bk {
+
+struct GptqArgs {
+    int64_t m, n;
+    int nt;           // column tiles
+    int64_t ldE;      // row stride of the error workspace (nt * 32)
+    const float* W;   // m x n row-major, not modified
+    const float* LA;  // packed unit-lower factor tiles
+    float* E;         // errors, ceil(m/16)*16 x nt*32 row-major (workspace)
+    QuantArgs q;
+    int8_t* codes;
+    float* V;
+    float* pre;       // may be null
+};
+
+__device__ inline f32x4 ld4(const float* p) { return *reinterpret_cast<const f32x4*>(p); }
+
+__device__ inline void mfma16_8(f32x4 a0, f32x4 a1, f32x4 b0, f32x4 b1, f32x4& acc) {
+#pragma unroll
+    for (int t = 0; t < 4; ++t) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a0[t], b0[t], acc, 0, 0, 0);
+#pragma unroll
+    for (int t = 0; t < 4; ++t) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a1[t], b1[t], acc, 0, 0, 0);
+}
+
+__global__ __launch_bounds__(256) void k_gptq(GptqArgs a) {
+    __shared__ float part[4][16][33];   // per wave: partial 16 x 32 lazy products
+    const int tid = threadIdx.x;
+    const int w = tid >> 6, l = tid & 63;
+    const int64_t row0 = (int64_t)blockIdx.x * 16;
+    // step 1 lane roles: A row i16, k chunk [8 s, 8 s + 8) of every source tile
+    const int i16 = l & 15, s = l >> 4;
+    // step 2 lane roles: row rr of the 16, block columns c16 and c16 + 16
+    const int rr = 4 * w + (l >> 4), c16 = l & 15;
+    const int64_t row = row0 + rr;
+    const float qlo = a.q.qlo, qhi = a.q.qhi;
+    const float nan = __builtin_nanf("");
+
+    for (int b = 0; b < a.nt; ++b) {
+        // 1. lazy feedback from the source tiles kt < b (a quarter per wave)
+        f32x4 acc0 = {0.0f, 0.0f, 0.0f, 0.0f}, acc1 = {0.0f, 0.0f, 0.0f, 0.0f};
+        {
+            const float* erow = a.E + (row0 + i16) * a.ldE + 8 * s;
+            const float* lt = a.LA + packed_tile_offset(b, 0) + i16 * TS + 8 * s;
+            int kt = w;
+            f32x4 ea0, ea1, la0, la1, lb0, lb1;
+            if (kt < b) {
+                ea0 = ld4(erow + kt * TS); ea1 = ld4(erow + kt * TS + 4);
+                la0 = ld4(lt + kt * TILE_ELEMS); la1 = ld4(lt + kt * TILE_ELEMS + 4);
+                lb0 = ld4(lt + kt * TILE_ELEMS + 16 * TS); lb1 = ld4(lt + kt * TILE_ELEMS + 16 * TS + 4);
+            }
+            for (; kt < b; kt += 4) {
+                const f32x4 x0 = ea0, x1 = ea1, y0 = la0, y1 = la1, z0 = lb0, z1 = lb1;
+                const int kn = kt + 4;
+                if (kn < b) {   // prefetch the next source tile of this wave
+                    ea0 = ld4(erow + kn * TS); ea1 = ld4(erow + kn * TS + 4);
+                    la0 = ld4(lt + kn * TILE_ELEMS); la1 = ld4(lt + kn * TILE_ELEMS + 4);
+                    lb0 = ld4(lt + kn * TILE_ELEMS + 16 * TS); lb1 = ld4(lt + kn * TILE_ELEMS + 16 * TS + 4);
+                }
+                mfma16_8(x0, x1, y0, y1, acc0);   // output columns 0..15 of the block
+                mfma16_8(x0, x1, z0, z1, acc1);   // output columns 16..31
+            }
+        }
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            part[w][4 * s + r][i16] = acc0[r];
+            part[w][4 * s + r][16 + i16] = acc1[r];
+        }
+        __syncthreads();
+
+        // 2. the block's 32 columns in order, 16 lanes per row
+        const int64_t col0 = (int64_t)b * TS + c16, col1 = col0 + 16;
+        float h0 = part[0][rr][c16] + part[1][rr][c16] + part[2][rr][c16] + part[3][rr][c16];
+        float h1 = part[0][rr][16 + c16] + part[1][rr][16 + c16] + part[2][rr][16 + c16] +
+                   part[3][rr][16 + c16];
+        if (row < a.m && col0 < a.n) h0 += a.W[row * a.n + col0];
+        if (row < a.m && col1 < a.n) h1 += a.W[row * a.n + col1];
+        const float s0 = entry_scale(a.q, row, col0, a.m, a.n);
+        const float s1 = entry_scale(a.q, row, col1, a.m, a.n);
+        const float is0 = s0 > 0.0f ? 1.0f / s0 : 0.0f;   // zero scale: alphabet {0}
+        const float is1 = s1 > 0.0f ? 1.0f / s1 : 0.0f;
+        // L^A[col][blk] of the lane's two columns, strictly below the diagonal
+        float c0[TS], c1[TS];
+        {
+            const float* d = a.LA + packed_tile_offset(b, b);
+#pragma unroll
+            for (int j = 0; j < TS; j += 4) {
+                const f32x4 u = ld4(d + c16 * TS + j), v = ld4(d + (16 + c16) * TS + j);
+#pragma unroll
+                for (int t = 0; t < 4; ++t) {
+                    c0[j + t] = (j + t < c16) ? u[t] : 0.0f;
+                    c1[j + t] = (j + t < 16 + c16) ? v[t] : 0.0f;
+                }
+            }
+        }
+        float e0 = 0.0f, e1 = 0.0f, x0 = 0.0f, x1 = 0.0f;
+#pragma unroll
+        for (int j = 0; j < TS; ++j) {
+            const bool hi = j >= 16;                       // column j sits in slot 1
+            const float hv = hi ? h1 : h0, iv = hi ? is1 : is0, sv = hi ? s1 : s0;
+            const float xv = hv * iv;
+            const float cq = __builtin_amdgcn_fmed3f(rintf(xv), qlo, qhi);
+            const float ev = fmaf(cq, sv, -hv);
+            // the owner of column j is lane (j & 15) of the row's 16 lanes
+            const float ej = __shfl(ev, (l & 48) | (j & 15), 64);
+            if (c16 == (j & 15)) {
+                if (hi) { e1 = ev; x1 = xv; } else { e0 = ev; x0 = xv; }
+            }
+            h0 = fmaf(ej, c0[j], h0);
+            h1 = fmaf(ej, c1[j], h1);
+        }
+        // errors for the later blocks (every workspace row and column is
+        // written, padding included: its errors are 0); outputs
+        a.E[row * a.ldE + col0] = e0;
+        a.E[row * a.ldE + col1] = e1;
+        if (row < a.m) {
+            if (col0 < a.n) {
+                const int64_t o = row * a.n + col0;
+                const float r = __builtin_amdgcn_fmed3f(rintf(x0), qlo, qhi);
+                a.codes[o] = (int8_t)(int)r;
+                a.V[o] = r * s0;
+                if (a.pre) a.pre[o] = s0 > 0.0f ? x0 : nan;
+            }
+            if (col1 < a.n) {
+                const int64_t o = row * a.n + col1;
+                const float r = __builtin_amdgcn_fmed3f(rintf(x1), qlo, qhi);
+                a.codes[o] = (int8_t)(int)r;
+                a.V[o] = r * s1;
+                if (a.pre) a.pre[o] = s1 > 0.0f ? x1 : nan;
+            }
+        }
+        __syncthreads();   // the block's errors and the partial sums are reused
+    }
+}
+
+size_t gptq_workspace_floats(int64_t m, int64_t n) {
+    return (size_t)((m + 15) / 16 * 16) * (size_t)((n + TS - 1) / TS * TS);
+}
+
+hipError_t run_gptq(hipStream_t st, const float* W, int64_t m, int64_t n, const float* LA, float* E,
+                    const QuantArgs& q, int8_t* codes, float* V, float* pre) {
+    GptqArgs a;
+    a.m = m;
+    a.n = n;
+    a.nt = (int)((n + TS - 1) / TS);
+    a.ldE = (int64_t)a.nt * TS;
+    a.W = W;
+    a.LA = LA;
+    a.E = E;
+    a.q = q;
+    a.codes = codes;
+    a.V = V;
+    a.pre = pre;
+    hipLaunchKernelGGL(k_gptq, dim3((unsigned)((m + 15) / 16)), dim3(256), 0, st, a);
+    return hipGetLastError();
+}
+
+}  // namespace bk

@@ -1,0 +1,97 @@
+"""B = NULL (B = I): the one-sided GPTQ kernel (Alg. 1 on every row with the
+Hessian A, blocked lazy updates on fp32 MFMA) against the fp64 oracle run
+with B = I, element by element under the tie-forced protocol; ragged shapes
+that span several 16-row groups and 32-column blocks, every quantiser
+variant, the two-sided solver forced with BAKRON_GPTQ=0 on the same inputs,
+determinism and a poisoned workspace."""
+import os
+
+import numpy as np
+import pytest
+
+import workloads
+from gpu_util import check_against_oracle, gpu_run, log
+
+pytestmark = pytest.mark.gpu
+
+
+def _problem(m, n, seed, bits=4):
+    return workloads.make_random(m, n, seed, bits=bits, identity_B=True)
+
+
+class _env:
+    def __init__(self, **kv):
+        self.kv = kv
+
+    def __enter__(self):
+        self.old = {k: os.environ.get(k) for k in self.kv}
+        os.environ.update({k: str(v) for k, v in self.kv.items()})
+
+    def __exit__(self, *a):
+        for k, v in self.old.items():
+            if v is None:
+                os.environ.pop(k, None)
+            else:
+                os.environ[k] = v
+
+
+@pytest.mark.parametrize("m,n", [(1, 1), (1, 37), (37, 1), (5, 37), (16, 32), (17, 33), (33, 65),
+                                 (130, 257), (257, 97), (64, 64)])
+def test_gptq_shapes(oracle_mod, m, n):
+    p = _problem(m, n, seed=500 + m + 7 * n)
+    log(f"case one-sided m={m} n={n}")
+    codes, V, pre = gpu_run(p)
+    check_against_oracle(p, codes, V, pre, oracle_mod, label=f"gptq{m}x{n}")
+
+
+@pytest.mark.parametrize("variant", ["bits2", "bits8", "asym+groups+cols", "zero-rows"])
+def test_gptq_quantisers(oracle_mod, variant):
+    m, n = 90, 150
+    p = _problem(m, n, seed=61, bits={"bits2": 2, "bits8": 8}.get(variant, 4))
+    if variant == "asym+groups+cols":
+        g = 32
+        rng = np.random.default_rng(5)
+        p["scale"] = (p["scale"][:, None] * rng.uniform(0.6, 1.4, (m, -(-n // g)))).astype(np.float32)
+        p["group_size"] = g
+        p["alphabet"] = "asym"
+        p["col_scale"] = rng.uniform(0.8, 1.25, n).astype(np.float32)
+    if variant == "zero-rows":
+        p["scale"] = p["scale"].copy()
+        p["scale"][[0, 45, 89]] = 0.0
+    log(f"case one-sided quantiser {variant}")
+    codes, V, pre = gpu_run(p)
+    check_against_oracle(p, codes, V, pre, oracle_mod, label=f"gptq-{variant}")
+
+
+def test_gptq_against_two_sided_solver(oracle_mod):
+    """The same B = I problem through the two-sided solver (BAKRON_GPTQ=0):
+    both agree with the oracle."""
+    p = _problem(200, 300, seed=62)
+    log("case one-sided vs two-sided solver")
+    with _env(BAKRON_GPTQ=0):
+        c2, v2, x2 = gpu_run(p, k=1)
+    check_against_oracle(p, c2, v2, x2, oracle_mod, label="two-sided-B=I")
+    c1, v1, x1 = gpu_run(p)
+    check_against_oracle(p, c1, v1, x1, oracle_mod, label="one-sided")
+    assert np.max(np.abs(x1.astype(np.float64) - x2)) < 1e-3
+
+
+def test_gptq_large_with_recursive_oracle(oracle_mod):
+    """1000 x 2080: many row groups and column blocks; the oracle replays the
+    sequence with Alg. 5 (same codes as Alg. 2)."""
+    p = _problem(1000, 2080, seed=63)
+    log("case one-sided 1000x2080")
+    codes, V, pre = gpu_run(p)
+    check_against_oracle(p, codes, V, pre, oracle_mod, label="gptq-1000x2080", method="recursive")
+
+
+def test_gptq_deterministic_and_poison_free():
+    p = _problem(150, 230, seed=64)
+    log("case one-sided determinism and poisoned workspace")
+    (c1, v1, x1), (c2, v2, x2) = gpu_run(p, repeat=2)
+    with _env(BAKRON_POISON=1):
+        c3, v3, x3 = gpu_run(p)
+    for c, v, x in ((c2, v2, x2), (c3, v3, x3)):
+        assert np.array_equal(c1, c)
+        assert np.array_equal(v1.view(np.uint32), v.view(np.uint32))
+        assert np.array_equal(np.nan_to_num(x1).view(np.uint32), np.nan_to_num(x).view(np.uint32))
