@@ -204,14 +204,16 @@ static void leaves(int K, int L, int knear, std::vector<std::pair<int, int>>& ou
 }
 
 // macro: 0 chooses the macro tile per node (128 x 128 when a node has at
-// least 512 such items, else 64 x 64); 4 or 2 forces one size
+// least 1536 such items, three rounds of the 512 that the chip holds at
+// once, else 64 x 64: with fewer, the last round of 128 x 128 items leaves
+// most CUs idle); 4 or 2 forces one size
 static bool node_op(int K, int Mid, int tlo, int thi, int mt, int nt, int knear, int b_ident,
                     std::vector<int4>& items, bk::PlanOp& op, int macro) {
     const double T = bk::TS;
     int MT = macro == 2 ? 2 : bk::MACRO;
     std::vector<int4> its;
     node_items(K, Mid, tlo, thi, mt, nt, knear, b_ident, MT, its);
-    if (macro == 0 && (int)its.size() < 512) {
+    if (macro == 0 && (int)its.size() < 1536) {
         MT = 2;
         node_items(K, Mid, tlo, thi, mt, nt, knear, b_ident, 2, its);
     }
