@@ -153,14 +153,19 @@ def normalized_factor(X, lam: float) -> np.ndarray:
     return Linv / np.diag(Linv)[None, :]
 
 
-def rev_cholesky(Xd) -> np.ndarray:
+def rev_cholesky(Xd, fortran: bool = False) -> np.ndarray:
     """Lower R with positive diagonal and R^T R = Xd (Sec. 3.1 definition).
 
     With P the reversal permutation, P Xd P = C C^T gives R = P C^T P.
-    """
+    C is LAPACK's fp64 Cholesky (dpotrf) of the column-major copy of P Xd P.
+    The result is row-major, or column-major with fortran=True."""
+    from scipy.linalg import lapack
     Xd = np.asarray(Xd, dtype=np.float64)
-    C = np.linalg.cholesky(Xd[::-1, ::-1])
-    return np.ascontiguousarray(C[::-1, ::-1].T)
+    C, info = lapack.dpotrf(np.asfortranarray(Xd[::-1, ::-1]), lower=1, clean=1, overwrite_a=1)
+    if info != 0:
+        raise np.linalg.LinAlgError(f"dpotrf info {info}: not positive definite")
+    R = C[::-1, ::-1].T
+    return np.asfortranarray(R) if fortran else np.ascontiguousarray(R)
 
 
 def babai(W, LA, LB, scale, bits: int, forced=None, tie_window: float = 0.0,
@@ -268,12 +273,15 @@ def normalized_factor_rev(X, lam: float) -> np.ndarray:
     R^-1 R^-T with R^-1 lower, so R^-1 D^-1 (D = diag(R^-1) = diag(R)^-1) is
     the Cholesky factor, and normalising its columns gives R^-1 diag(R)."""
     from scipy.linalg import lapack
-    R = rev_cholesky(damp(X, lam))
-    Rinv, info = lapack.dtrtri(R, lower=1)
+    R = rev_cholesky(damp(X, lam), fortran=True)
+    d = np.diag(R).copy()
+    Rinv, info = lapack.dtrtri(R, lower=1, overwrite_c=1)
     if info != 0:
         raise np.linalg.LinAlgError(f"dtrtri info {info}")
-    Rinv = np.tril(Rinv)
-    return Rinv * np.diag(R)[None, :]
+    del R
+    L = np.tril(Rinv)
+    L *= d[None, :]
+    return np.ascontiguousarray(L)
 
 
 def solve(W, A, B, damp_lambda: float, scale, bits: int, forced=None,
