@@ -609,7 +609,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="with --factors: seconds of oracle work for its CPU baseline")
-    ap.add_argument("--cpu-rows", type=int, default=8192,
+    ap.add_argument("--cpu-rows", type=int, default=12288,
                     help="rows of the layer sample the CPU baseline solves (oracle, Alg. 5)")
     ap.add_argument("--cpu-full", action="store_true",
                     help="only time the fp64 oracle (Alg. 5) on the whole configured layer on the "

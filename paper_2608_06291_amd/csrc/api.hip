@@ -588,8 +588,27 @@ static double plan_model_seconds(const bk::Plan& p, int cus_main, int cus_side) 
     return std::max(tm, ts);
 }
 
+// first CU of the side stream on a device with ncu CUs (the main stream
+// keeps at least half of them and one CU per strip of the widest segment),
+// or 0 when fewer than 64 CUs would be left for the side stream
+static int side_split(const bk::Plan& one, int ncu) {
+    int widest = 0;
+    for (const bk::PlanOp& op : one.ops)
+        if (op.kind == 0) widest = imax(widest, op.nstrips);
+    const int R = imax(ncu / 2, (widest + 31) / 32 * 32);
+    return (ncu > 0 && ncu - R >= 64) ? R : 0;
+}
+
 // defer: 0 never, 1 whenever enough CUs are free, 2 when the modelled
 // duration of the two-stream plan is below that of the one-stream plan
+static bool use_two_streams(const bk::Plan& one, const bk::Plan& two, int R, int ncu, int defer) {
+    if (R <= 0 || two.side.empty() || defer == 0) return false;
+    // the overlap pays only while the pushes into later segments fit on
+    // the side CUs during the chain; with more push work (tall or wide
+    // layers) one stream with every CU per push is faster
+    return defer == 1 || plan_model_seconds(two, R, ncu - R) < plan_model_seconds(one, ncu, 0);
+}
+
 static bakron_status build_plan_entry(bakron_factors* f, int mt, int nt, int defer,
                                       PlanEntry& pe) {
     std::vector<int4> items_host;
@@ -598,21 +617,13 @@ static bakron_status build_plan_entry(bakron_factors* f, int mt, int nt, int def
     int ncu = 0;
     hipDeviceProp_t prop;
     if (defer && hipGetDeviceProperties(&prop, f->device) == hipSuccess) ncu = prop.multiProcessorCount;
-    int widest = 0;
-    for (const bk::PlanOp& op : pe.plan[0].ops)
-        if (op.kind == 0) widest = imax(widest, op.nstrips);
-    const int R = imax(ncu / 2, (widest + 31) / 32 * 32);
-    if (ncu > 0 && ncu - R >= 64) {
+    const int R = side_split(pe.plan[0], ncu);
+    if (R > 0) {
         bk::Plan deferred;
         std::vector<int4> items;
         build_plan(mt, nt, f->knear, f->b_ident, true, deferred, items, f->macro);
         deferred.side_cu_lo = R;
-        // the overlap pays only while the pushes into later segments fit on
-        // the side CUs during the chain; with more push work (tall or wide
-        // layers) one stream with every CU per push is faster
-        const bool use = !deferred.side.empty() &&
-                         (defer == 1 || plan_model_seconds(deferred, R, ncu - R) <
-                                            plan_model_seconds(pe.plan[0], ncu, 0));
+        const bool use = use_two_streams(pe.plan[0], deferred, R, ncu, defer);
         if (use && masked_streams(f->device, ncu, R, &pe.main, &pe.side)) {
             const int off = (int)items_host.size();
             for (bk::PlanOp& op : deferred.ops) if (op.kind == 1) op.item_off += off;

@@ -93,16 +93,38 @@ int main() {
     for (auto& sh : small) for (int k : {0, 1, 3, 8}) for (int bi : {0, 1}) for (int d : {0, 1})
         fails += check(sh[0], sh[1], k, bi, d);
     for (int k : {1, 8}) for (int d : {0, 1}) fails += check(128, 128, k, 0, d);   // the 4096^2 layer
-    // the cost model's choice on 256 CUs, as measured on MI355X: the overlap
-    // for the 4096^2 layer (main CUs 0-127), one stream for 11008 x 4096
-    // and 8192 x 2048 (overlap 1.7x and 1.6x slower)
-    int shapes[3][3] = {{128, 128, 1}, {344, 128, 0}, {256, 64, 0}};
+    // the library's choice on 256 CUs against the faster plan measured on
+    // MI355X for each shape (tiles of 32; solve ms with one stream / two):
+    // 1 = two streams, 0 = one stream, -1 = within 1% (either is accepted)
+    int shapes[][3] = {
+        {128, 128, 1},    // 4096 x 4096:   4.98 / 4.74
+        {96, 96, -1},     // 3072 x 3072:   3.52 / 3.48
+        {256, 64, 0},     // 8192 x 2048:   6.61 / 10.61
+        {64, 256, 0},     // 2048 x 8192:   6.54 / 10.54
+        {344, 128, 0},    // 11008 x 4096: 12.99 / 22.09
+        {128, 344, 0},    // 4096 x 11008: 12.77 / 20.29
+        {448, 128, 0},    // 14336 x 4096: 17.87 / 24.17
+        {128, 448, 0},    // 4096 x 14336: 17.24 / 27.96
+        {256, 128, 0},    // 8192 x 4096:   9.58 / 17.35
+        {128, 256, 0},    // 4096 x 8192:   9.48 / 14.51
+        {160, 160, 0},    // 5120 x 5120:   7.51 / 10.72
+        {192, 192, 0},    // 6144 x 6144:  10.23 / 22.86
+        {896, 256, 0},    // 28672 x 8192: the widest segment needs every CU
+    };
     for (auto& sh : shapes) {
         bk::Plan p0, p1; std::vector<int4> it;
         build_plan(sh[0], sh[1], 8, 0, false, p0, it);
-        build_plan(sh[0], sh[1], 8, 0, true, p1, it);
-        const bool two = plan_model_seconds(p1, 128, 128) < plan_model_seconds(p0, 256, 0);
-        if (two != (sh[2] != 0)) { printf("cost model picks the wrong plan for %dx%d tiles\n", sh[0], sh[1]); ++fails; }
+        const int R = side_split(p0, 256);
+        bool two = false;
+        if (R > 0) {
+            build_plan(sh[0], sh[1], 8, 0, true, p1, it);
+            two = use_two_streams(p0, p1, R, 256, 2);
+        }
+        printf("%dx%d tiles: %s stream plan\n", sh[0], sh[1], two ? "two" : "one");
+        if (sh[2] >= 0 && two != (sh[2] != 0)) {
+            printf("cost model picks the slower plan for %dx%d tiles\n", sh[0], sh[1]);
+            ++fails;
+        }
     }
     printf("fails %d\n", fails);
     return fails;
