@@ -148,7 +148,8 @@ constexpr int PULL_T0 = 2;        // first loop turn whose idle waves may consum
 //     128-byte rows with device-coherent (sc1) 16-byte stores, which the
 //     memory system acknowledges much sooner than scattered 4-byte ones; wait
 //     for them, set the tile's flag.  E goes to the ring and to X (read by the
-//     node launches after this one); then codes, V and pre.
+//     node launches after this one);
+//  4. codes, V and pre, gathered in LDS and written as row segments.
 //
 // In-tile rounding: each thread owns two entries of one row p: slot 0 at
 // column q0 and slot 1 at column q1 = q0 + 1 (mod 32), so p + q1 = p + q0 + 1.
@@ -179,6 +180,7 @@ __global__ __launch_bounds__(512) void k_seg(SegArgs a) {
     __shared__ __attribute__((aligned(16))) float LBn[KNEAR_MAX][TILE_ELEMS];      // L^B[I', I'-k-1]
     __shared__ __attribute__((aligned(16))) float Yn[KNEAR_MAX - 1][TILE_ELEMS];   // F[I', J-k-2]
     __shared__ __attribute__((aligned(16))) float Fst[TS][RSTR];   // F of the tile, row-major
+    __shared__ float So[GQ ? TS : 1][TS + 1];   // scales of the tile's entries (per row without GQ)
     __shared__ int tk, ynext;
 
     const int tid = threadIdx.x;
@@ -271,7 +273,6 @@ __global__ __launch_bounds__(512) void k_seg(SegArgs a) {
             }
             float h0 = pf_h0, h1 = pf_h1;
             float g0 = pf_g0, g1 = pf_g1;
-            const int row = I * TS + p;
             // scales of the thread's two entries (one per row without GQ)
             const float s0 = pf_s0, s1 = GQ ? pf_s1 : s0;
             const float inv_s0 = (s0 > 0.0f) ? 1.0f / s0 : 0.0f;
@@ -489,22 +490,52 @@ __global__ __launch_bounds__(512) void k_seg(SegArgs a) {
             if (tid == 0)
                 __hip_atomic_store(a.flags + I * a.nt + J, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 
-            const float nan = __builtin_nanf("");
-            const int64_t col0 = (int64_t)J * TS + q0, col1 = (int64_t)J * TS + q1;
-            if (row < a.m) {
-                if (col0 < a.n) {
-                    const int64_t o = (int64_t)row * a.n + col0;
-                    const float r = __builtin_amdgcn_fmed3f(rintf(xv0), qlo, qhi);
-                    a.codes[o] = (int8_t)(int)r;
-                    a.V[o] = r * s0;
-                    if (a.pre) a.pre[o] = s0 > 0.0f ? xv0 : nan;
+            // 4. outputs, as whole row segments: every thread leaves x and the
+            // scale of its entries in LDS (F is stored, Fst is free), then 256
+            // threads write 4 consecutive entries of one row each (one 4-byte
+            // code store and 16-byte V and pre stores instead of 64 scattered
+            // rows per instruction)
+            Fst[p][q0] = xv0;
+            Fst[p][q1] = xv1;
+            if (GQ) {
+                So[p][q0] = s0;
+                So[p][q1] = s1;
+            } else {
+                So[0][p] = s0;
+            }
+            __syncthreads();
+            if (tid < 256) {
+                const float nan = __builtin_nanf("");
+                const int r = tid >> 3, cb = 4 * (tid & 7);
+                const int64_t orow = (int64_t)I * TS + r, ocol = (int64_t)J * TS + cb;
+                const f32x4 xq = *reinterpret_cast<const f32x4*>(&Fst[r][cb]);
+                float cv[4], vv[4], pv[4];
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    const float sk = GQ ? So[r][cb + k] : So[0][r];
+                    cv[k] = __builtin_amdgcn_fmed3f(rintf(xq[k]), qlo, qhi);
+                    vv[k] = cv[k] * sk;
+                    pv[k] = sk > 0.0f ? xq[k] : nan;
                 }
-                if (col1 < a.n) {
-                    const int64_t o = (int64_t)row * a.n + col1;
-                    const float r = __builtin_amdgcn_fmed3f(rintf(xv1), qlo, qhi);
-                    a.codes[o] = (int8_t)(int)r;
-                    a.V[o] = r * s1;
-                    if (a.pre) a.pre[o] = s1 > 0.0f ? xv1 : nan;
+                if (orow < a.m) {
+                    const int64_t o = orow * a.n + ocol;
+                    if ((a.n & 3) == 0 && ocol + 3 < a.n) {   // aligned, inside the matrix
+                        uint32_t packed = 0;
+#pragma unroll
+                        for (int k = 0; k < 4; ++k) packed |= (uint32_t)(uint8_t)(int8_t)(int)cv[k] << (8 * k);
+                        *reinterpret_cast<uint32_t*>(a.codes + o) = packed;
+                        *reinterpret_cast<f32x4*>(a.V + o) = f32x4{vv[0], vv[1], vv[2], vv[3]};
+                        if (a.pre) *reinterpret_cast<f32x4*>(a.pre + o) = f32x4{pv[0], pv[1], pv[2], pv[3]};
+                    } else {
+#pragma unroll
+                        for (int k = 0; k < 4; ++k) {
+                            if (ocol + k < a.n) {
+                                a.codes[o + k] = (int8_t)(int)cv[k];
+                                a.V[o + k] = vv[k];
+                                if (a.pre) a.pre[o + k] = pv[k];
+                            }
+                        }
+                    }
                 }
             }
         }
