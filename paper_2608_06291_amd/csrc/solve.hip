@@ -252,7 +252,7 @@ __global__ __launch_bounds__(512) void k_seg(SegArgs a) {
             // address of the unrolled loop below live across tiles
             int tid = threadIdx.x;
             asm volatile("" : "+v"(tid));
-            const int w = (int)threadIdx.x >> 6, l = tid & 63;   // w: wave-uniform
+            const int w = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6), l = tid & 63;   // w: wave-uniform
             const int hf = l >> 5;
             const int p = l & 31;
             const int c0 = 4 * w + 2 * hf;
@@ -300,14 +300,19 @@ __global__ __launch_bounds__(512) void k_seg(SegArgs a) {
             // k = 1..min(knear, It), and F[It, J-k], k = 2..kr
             auto stage = [&](int It, bool lb, bool y) {
                 const int nlb = lb ? (knear < It ? knear : It) : 0;
-                const int ny = y ? kr - 1 : 0;
-                for (int g = w; g < 4 * (nlb + ny); g += 8) {
-                    const int ti = g >> 2;
-                    if (ti < nlb)
-                        stage_rows<0>(a.LB + packed_tile_offset(It, It - 1 - ti), LBn[ti], g & 3, l);
-                    else
-                        stage_rows<CPOL_SC1>(a.Y + ws_tile_offset(It, J - 2 - (ti - nlb), a.nt),
-                                             Yn[ti - nlb], g & 3, l);
+                const int lim = 4 * (nlb + (y ? kr - 1 : 0));
+                // wave w issues row groups g = w, w + 8, ... (uniform control flow)
+#pragma unroll
+                for (int i = 0; i < (4 * (2 * KNEAR_MAX - 1) + 7) / 8; ++i) {
+                    const int g = w + 8 * i;
+                    if (g < lim) {
+                        const int ti = g >> 2;
+                        if (ti < nlb)
+                            stage_rows<0>(a.LB + packed_tile_offset(It, It - 1 - ti), LBn[ti], g & 3, l);
+                        else
+                            stage_rows<CPOL_SC1>(a.Y + ws_tile_offset(It, J - 2 - (ti - nlb), a.nt),
+                                                 Yn[ti - nlb], g & 3, l);
+                    }
                 }
             };
 
