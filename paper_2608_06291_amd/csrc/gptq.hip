@@ -16,10 +16,11 @@
 // A workgroup owns 16 rows and walks all column blocks.  In step 1 each of
 // its 4 waves multiplies a quarter of the source tiles (tile kt = w, w + 4,
 // ...) with v_mfma_f32_16x16x4f32 (A = the 16 error rows, B = the factor tile
-// rows, so D[i][j] = sum_k E[i][k] L^A[j][k]); the four partial sums meet in
-// LDS.  In step 2 each wave owns 4 rows, 16 lanes per row with the block
-// columns c and c + 16 in registers; the error of column j is broadcast along
-// its 16 lanes with a lane shuffle, so no barrier is needed inside the block.
+// rows, so D[i][j] = sum_k E[i][k] L^A[j][k]), with the operands of its next
+// two tiles in flight; the four partial sums meet in LDS.  In step 2 each
+// wave owns 4 rows, 16 lanes per row with the block columns c and c + 16 in
+// registers; the error of column j is broadcast along its 16 lanes with a
+// lane shuffle, so no barrier is needed inside the block.
 #include "common.h"
 
 namespace bk {
@@ -46,10 +47,12 @@ __device__ inline void mfma16_8(f32x4 a0, f32x4 a1, f32x4 b0, f32x4 b1, f32x4& a
     for (int t = 0; t < 4; ++t) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a1[t], b1[t], acc, 0, 0, 0);
 }
 
-__global__ __launch_bounds__(256) void k_gptq(GptqArgs a) {
-    __shared__ float part[4][16][33];   // per wave: partial 16 x 32 lazy products
+constexpr int GW = 4;   // waves per workgroup
+
+__global__ __launch_bounds__(64 * GW) void k_gptq(GptqArgs a) {
+    __shared__ float part[GW][16][33];   // per wave: partial 16 x 32 lazy products
     const int tid = threadIdx.x;
-    const int w = tid >> 6, l = tid & 63;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6), l = tid & 63;
     const int64_t row0 = (int64_t)blockIdx.x * 16;
     // step 1 lane roles: A row i16, k chunk [8 s, 8 s + 8) of every source tile
     const int i16 = l & 15, s = l >> 4;
@@ -60,29 +63,44 @@ __global__ __launch_bounds__(256) void k_gptq(GptqArgs a) {
     const float nan = __builtin_nanf("");
 
     for (int b = 0; b < a.nt; ++b) {
-        // 1. lazy feedback from the source tiles kt < b (a quarter per wave)
+        // 1. lazy feedback from the source tiles kt < b (a quarter per wave),
+        // two tiles in flight: set 0 holds tiles w, w + 2 GW, ..., set 1
+        // tiles w + GW, w + 3 GW, ...
         f32x4 acc0 = {0.0f, 0.0f, 0.0f, 0.0f}, acc1 = {0.0f, 0.0f, 0.0f, 0.0f};
         {
             const float* erow = a.E + (row0 + i16) * a.ldE + 8 * s;
             const float* lt = a.LA + packed_tile_offset(b, 0) + i16 * TS + 8 * s;
+            f32x4 e0[2], e1[2], l0[2], l1[2], m0[2], m1[2];
+            auto ld = [&](int kt, int q) {
+                e0[q] = ld4(erow + kt * TS);
+                e1[q] = ld4(erow + kt * TS + 4);
+                l0[q] = ld4(lt + kt * TILE_ELEMS);
+                l1[q] = ld4(lt + kt * TILE_ELEMS + 4);
+                m0[q] = ld4(lt + kt * TILE_ELEMS + 16 * TS);
+                m1[q] = ld4(lt + kt * TILE_ELEMS + 16 * TS + 4);
+            };
+            auto mul = [&](int q) {
+                mfma16_8(e0[q], e1[q], l0[q], l1[q], acc0);   // output columns 0..15 of the block
+                mfma16_8(e0[q], e1[q], m0[q], m1[q], acc1);   // output columns 16..31
+            };
             int kt = w;
-            f32x4 ea0, ea1, la0, la1, lb0, lb1;
-            if (kt < b) {
-                ea0 = ld4(erow + kt * TS); ea1 = ld4(erow + kt * TS + 4);
-                la0 = ld4(lt + kt * TILE_ELEMS); la1 = ld4(lt + kt * TILE_ELEMS + 4);
-                lb0 = ld4(lt + kt * TILE_ELEMS + 16 * TS); lb1 = ld4(lt + kt * TILE_ELEMS + 16 * TS + 4);
-            }
-            for (; kt < b; kt += 4) {
-                const f32x4 x0 = ea0, x1 = ea1, y0 = la0, y1 = la1, z0 = lb0, z1 = lb1;
-                const int kn = kt + 4;
-                if (kn < b) {   // prefetch the next source tile of this wave
-                    ea0 = ld4(erow + kn * TS); ea1 = ld4(erow + kn * TS + 4);
-                    la0 = ld4(lt + kn * TILE_ELEMS); la1 = ld4(lt + kn * TILE_ELEMS + 4);
-                    lb0 = ld4(lt + kn * TILE_ELEMS + 16 * TS); lb1 = ld4(lt + kn * TILE_ELEMS + 16 * TS + 4);
+            if (kt < b) ld(kt, 0);
+            if (kt + GW < b) ld(kt + GW, 1);
+            for (; kt + GW < b; kt += 2 * GW) {
+                {
+                    const f32x4 x0 = e0[0], x1 = e1[0], y0 = l0[0], y1 = l1[0], z0 = m0[0], z1 = m1[0];
+                    if (kt + 2 * GW < b) ld(kt + 2 * GW, 0);
+                    mfma16_8(x0, x1, y0, y1, acc0);
+                    mfma16_8(x0, x1, z0, z1, acc1);
                 }
-                mfma16_8(x0, x1, y0, y1, acc0);   // output columns 0..15 of the block
-                mfma16_8(x0, x1, z0, z1, acc1);   // output columns 16..31
+                {
+                    const f32x4 x0 = e0[1], x1 = e1[1], y0 = l0[1], y1 = l1[1], z0 = m0[1], z1 = m1[1];
+                    if (kt + 3 * GW < b) ld(kt + 3 * GW, 1);
+                    mfma16_8(x0, x1, y0, y1, acc0);
+                    mfma16_8(x0, x1, z0, z1, acc1);
+                }
             }
+            if (kt < b) mul(0);
         }
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
@@ -93,9 +111,12 @@ __global__ __launch_bounds__(256) void k_gptq(GptqArgs a) {
 
         // 2. the block's 32 columns in order, 16 lanes per row
         const int64_t col0 = (int64_t)b * TS + c16, col1 = col0 + 16;
-        float h0 = part[0][rr][c16] + part[1][rr][c16] + part[2][rr][c16] + part[3][rr][c16];
-        float h1 = part[0][rr][16 + c16] + part[1][rr][16 + c16] + part[2][rr][16 + c16] +
-                   part[3][rr][16 + c16];
+        float h0 = part[0][rr][c16], h1 = part[0][rr][16 + c16];
+#pragma unroll
+        for (int v = 1; v < GW; ++v) {
+            h0 += part[v][rr][c16];
+            h1 += part[v][rr][16 + c16];
+        }
         if (row < a.m && col0 < a.n) h0 += a.W[row * a.n + col0];
         if (row < a.m && col1 < a.n) h1 += a.W[row * a.n + col1];
         const float s0 = entry_scale(a.q, row, col0, a.m, a.n);
@@ -174,7 +195,7 @@ hipError_t run_gptq(hipStream_t st, const float* W, int64_t m, int64_t n, const 
     a.codes = codes;
     a.V = V;
     a.pre = pre;
-    hipLaunchKernelGGL(k_gptq, dim3((unsigned)((m + 15) / 16)), dim3(256), 0, st, a);
+    hipLaunchKernelGGL(k_gptq, dim3((unsigned)((m + 15) / 16)), dim3(64 * GW), 0, st, a);
     return hipGetLastError();
 }
 
