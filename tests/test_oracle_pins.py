@@ -90,6 +90,34 @@ def test_explicit_kronecker_hessian(oracle_mod, m, n):
     assert np.array_equal(got, ref)
 
 
+def test_explicit_kronecker_hessian_config1(oracle_mod):
+    """The 64 x 64 configuration itself: Alg. 1 on vec(W) with the explicit
+    4096 x 4096 Hessian A_d (x) B_d and its own Cholesky(H^-1) gives the codes
+    of the 2-D oracle (Alg. 2) on every entry, and the same pre-rounding
+    values up to fp64 rounding."""
+    import workloads
+    o = oracle_mod
+    c = workloads.make(1, seed=0)
+    W = c["W"].astype(np.float64)
+    m, n = W.shape
+    Ad, Bd = o.damp(c["A"], c["damp"]), o.damp(c["B"], c["damp"])
+    H = np.kron(Ad, Bd)
+    L = np.linalg.cholesky(np.linalg.inv(H))
+    L = L / np.diag(L)[None, :]
+    w = W.reshape(-1, order="F").copy()
+    svec = np.tile(c["scale"].astype(np.float64), n)
+    from oracle.oracle import quantise_codes
+    codes = np.zeros(m * n, np.int8)
+    x = np.zeros(m * n)
+    for i in range(m * n):
+        x[i] = w[i] / svec[i]
+        codes[i] = int(quantise_codes(np.array([x[i]]), c["bits"])[0])
+        w[i + 1:] += (svec[i] * codes[i] - w[i]) * L[i + 1:, i]
+    got = o.solve(W, c["A"], c["B"], c["damp"], c["scale"], c["bits"])
+    assert np.array_equal(got["codes"], codes.reshape((m, n), order="F"))
+    assert np.max(np.abs(got["pre"] - x.reshape((m, n), order="F"))) < 1e-8
+
+
 @pytest.mark.parametrize("m,n", [(2, 3), (3, 3), (4, 5)])
 def test_obs_constrained_reminimisation(oracle_mod, m, n):
     """Sec. 3.2 OBS view: after fixing the processed set S, the free entries F
