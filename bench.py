@@ -39,6 +39,26 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
+def device_peak() -> dict:
+    """CU count and peak clock of device 0 as the HIP runtime reports them,
+    and the fp32 MFMA peak they imply (256 flop per clock per CU); the
+    published 157.3 TFLOP/s is what `frac` uses."""
+    import ctypes
+    out = {}
+    try:
+        hip = ctypes.CDLL("libamdhip64.so")
+        v = ctypes.c_int()
+        # hipDeviceAttributeMultiprocessorCount = 63, hipDeviceAttributeClockRate = 5 (kHz)
+        for name, attr in (("cus", 63), ("peak_clock_khz", 5)):
+            if hip.hipDeviceGetAttribute(ctypes.byref(v), attr, 0) == 0:
+                out[name] = v.value
+    except OSError:
+        return out
+    if "cus" in out and "peak_clock_khz" in out:
+        out["fp32_mfma_peak_tflops"] = out["cus"] * 256 * out["peak_clock_khz"] * 1e3 / 1e12
+    return out
+
+
 def cpu_model() -> str:
     try:
         for line in open("/proc/cpuinfo"):
@@ -818,7 +838,7 @@ def main():
                    "seed": args.seed, "counted_flops": F, "ms_per_layer": ms,
                    "frac_fp32_mfma_peak": tflops / PEAK_FP32_MFMA, "factor_ms": factor_ms,
                    "end_to_end_ms": factor_ms + ms, "profiled_ms_per_step": prof_ms / P,
-                   "validation": validation,
+                   "validation": validation, "device": device_peak(),
                    "vs_baseline_note": ("paper Table 3, 4096x4096 in 0.288 s on one RTX PRO 6000 "
                                         "fp32 (other hardware, unspecified matrix contents)")
                    if vs is not None else None},

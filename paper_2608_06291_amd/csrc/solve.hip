@@ -206,19 +206,20 @@ __global__ __launch_bounds__(512) void k_seg(SegArgs a) {
         const bool need_y = kr >= 2;
 
         // strip set-up: L^A[J, J] and L^A[J, J-k], the ring with the errors of
-        // the tiles above that were solved by earlier launches
-        for (int e = tid; e < TILE_ELEMS; e += 512) LAt[e >> 5][e & 31] = a.LA[packed_tile_offset(J, J) + e];
+        // the tiles above that were solved by earlier launches, the first
+        // tile's inputs and its staged pull operands.  Every load is issued
+        // before any is waited for: one memory round trip per strip.
+        const int npre = a.b_ident ? 0 : (knear < I_first ? knear : I_first);
+        float2 rg[KNEAR_MAX];
+#pragma unroll
+        for (int k = 0; k < KNEAR_MAX; ++k)
+            if (k < npre)   // uniform
+                rg[k] = *reinterpret_cast<const float2*>(a.X + ws_tile_offset(I_first - 1 - k, J, a.nt) +
+                                                          2 * tid);   // E^T, column-major E
+        const float lat0 = a.LA[packed_tile_offset(J, J) + tid];
+        const float lat1 = a.LA[packed_tile_offset(J, J) + tid + 512];
         for (int g = w; g < 4 * kr; g += 8)
             stage_rows<0>(a.LA + packed_tile_offset(J, J - 1 - (g >> 2)), LAs[g >> 2], g & 3, l);
-        if (!a.b_ident) {
-            const int npre = knear < I_first ? knear : I_first;
-            for (int k = 1; k <= npre; ++k) {
-                const float* src = a.X + ws_tile_offset(I_first - k, J, a.nt);   // E^T, column-major E
-                float (*ring)[RSTR] = Ering[(I_first - k) % RING];
-                for (int e = tid; e < TILE_ELEMS; e += 512) ring[e >> 5][e & 31] = src[e];
-            }
-        }
-        __syncthreads();
 
         // inputs of the first tile; later tiles' inputs are prefetched during
         // the previous tile's rounding loop
@@ -239,10 +240,40 @@ __global__ __launch_bounds__(512) void k_seg(SegArgs a) {
             pf_s0 = row_scale_of<GQ>(a.q, row, cs0, a.m);
             pf_s1 = GQ ? row_scale_of<GQ>(a.q, row, cs1, a.m) : 0.0f;
         }
+        // the first tile's pull operands: L^B[I_first, I_first - k] and the
+        // left strips' F[I_first, J - k], k >= 2 (after the flag of
+        // (I_first, J - 2), which stands for the whole row to its left)
+        {
+            const int nlb = npre;
+            if (need_y) wait_ready(a.flags + I_first * a.nt + (J - 2), a.status, a.spin_limit);
+            const int lim = 4 * (nlb + (need_y ? kr - 1 : 0));
+            const int wu = __builtin_amdgcn_readfirstlane(w);
+            __atomic_signal_fence(__ATOMIC_SEQ_CST);   // the F loads stay after the flag test
+#pragma unroll
+            for (int i = 0; i < (4 * (2 * KNEAR_MAX - 1) + 7) / 8; ++i) {
+                const int g = wu + 8 * i;
+                if (g < lim) {
+                    const int ti = g >> 2;
+                    if (ti < nlb)
+                        stage_rows<0>(a.LB + packed_tile_offset(I_first, I_first - 1 - ti), LBn[ti], g & 3, l);
+                    else
+                        stage_rows<CPOL_SC1>(a.Y + ws_tile_offset(I_first, J - 2 - (ti - nlb), a.nt),
+                                             Yn[ti - nlb], g & 3, l);
+                }
+            }
+        }
+        LAt[tid >> 5][tid & 31] = lat0;
+        LAt[(tid + 512) >> 5][tid & 31] = lat1;
+#pragma unroll
+        for (int k = 0; k < KNEAR_MAX; ++k)
+            if (k < npre)
+                *reinterpret_cast<float2*>(&Ering[(I_first - 1 - k) % RING][(2 * tid) >> 5][(2 * tid) & 31]) = rg[k];
+        __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0): this wave's direct loads landed
+        __syncthreads();
 
         // pull state of the next tile (uniform): which operands are staged,
         // and per wave the next source distance to multiply
-        bool lb_staged = false, y_staged = false;
+        bool lb_staged = true, y_staged = true;   // the first tile's, above
         int nk = 2;
         f32x4 pacc = {0.0f, 0.0f, 0.0f, 0.0f};
 
@@ -320,7 +351,7 @@ __global__ __launch_bounds__(512) void k_seg(SegArgs a) {
             // (first tile of the strip, or a left strip that was late) are
             // staged now.
             const bool lb_need = !a.b_ident && kc >= 1;
-            if ((lb_need && !lb_staged) || (need_y && !y_staged) || I == I_first) {   // uniform
+            if ((lb_need && !lb_staged) || (need_y && !y_staged)) {   // uniform
                 if (need_y && !y_staged) wait_ready(a.flags + I * a.nt + (J - 2), a.status, a.spin_limit);
                 stage(I, lb_need && !lb_staged, need_y && !y_staged);
                 __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0): this wave's direct loads landed
