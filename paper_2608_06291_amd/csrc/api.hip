@@ -563,7 +563,7 @@ static bool masked_streams(int device, int ncu, int R, hipStream_t* main, hipStr
 // (3072^2 to 14336 x 4096) under both plans; only the comparison of the two
 // plans for one shape uses them.
 static double plan_model_seconds(const bk::Plan& p, int cus_main, int cus_side) {
-    const double t_diag = 14.2e-6, t_seg = 3e-6, t_node = 6e-6, t_side = 30e-6, t_wait = 40e-6;
+    const double t_diag = 13.4e-6, t_seg = 3e-6, t_node = 6e-6, t_side = 30e-6, t_wait = 40e-6;
     const double rate_cu = 0.45e12;
     std::vector<double> main_end(p.ops.size(), 0.0), side_end(p.side.size(), 0.0);
     double tm = 0.0, ts = 0.0;
