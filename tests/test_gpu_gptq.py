@@ -95,3 +95,29 @@ def test_gptq_deterministic_and_poison_free():
         assert np.array_equal(c1, c)
         assert np.array_equal(v1.view(np.uint32), v.view(np.uint32))
         assert np.array_equal(np.nan_to_num(x1).view(np.uint32), np.nan_to_num(x).view(np.uint32))
+
+
+@pytest.mark.timeout(600)
+def test_gptq_certificate_wide_table3_shape(oracle_mod):
+    """A Table 3 shape with the longest sequential chain per row, 2048 x 8192
+    (A the AR(1) Toeplitz matrix rho^|i-j| with rho = 0.5, W ~ N(0, 0.02^2),
+    INT4 per-row scales, 1% damping, B = I): the certificate (closed form of
+    Eq. (1)) along the kernel's own trajectory, on every entry, and the
+    objective."""
+    import json
+    o = oracle_mod
+    m, n = 2048, 8192
+    rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([3000, m, n])))
+    W = (rng.standard_normal((m, n)) * 0.02).astype(np.float32)
+    p = dict(W=W, A=workloads.ar1_toeplitz(n, 0.5), B=None, scale=workloads.row_scales(W, 4), bits=4,
+             damp=0.01)
+    log("case one-sided 2048x8192 certificate")
+    codes, V, pre = gpu_run(p)
+    cert = o.certify(p["W"], p["A"], None, p["damp"], p["scale"], codes, p["bits"], window=1e-4)
+    v, x = cert["verdict"], cert["x"]
+    fin = np.isfinite(x)
+    margin = float(np.max(np.abs(pre[fin].astype(np.float64) - x[fin])))
+    log("[gptq-2048x8192] " + json.dumps(dict(**v, margin_grid_steps=margin, objective=cert["objective"])))
+    assert v["violations"] == 0
+    assert v["flips"] <= 1e-4 * m * n
+    assert margin < 1e-4
