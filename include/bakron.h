@@ -119,8 +119,9 @@ bakron_status bakron_factor(const float *A, int64_t n, const float *B, int64_t m
  *   V      device, m x n fp32 output, V_ij = s_ij * codes_ij (one fp32 product)
  *
  * The first call for a given (m, n) allocates the workspace (about 8*m*n
- * bytes plus one int per 32 x 32 tile) and builds the launch plans; later
- * calls with the same (m, n) allocate nothing and never synchronise the host.
+ * bytes plus one int per 32 x 32 tile) and builds the launch plans (and may
+ * synchronise the host, see below); later calls with the same (m, n)
+ * allocate nothing and never synchronise the host.
  * The work is ordered after everything enqueued on `stream` before the call,
  * and everything enqueued on `stream` after it is ordered after the solve.
  * On a stream other than the legacy default stream (0 / hipStreamLegacy) the
@@ -130,7 +131,11 @@ bakron_status bakron_factor(const float *A, int64_t n, const float *B, int64_t m
  * for the shapes where a cost model of both schedules, built when the shape
  * is first planned, favours the overlap (near-square layers up to about
  * 4096 x 4096), always with the environment variable BAKRON_DEFER=1, and
- * never with BAKRON_DEFER=0.  On the legacy default stream, which
+ * never with BAKRON_DEFER=0.  When the cost model picks the two-stream plan
+ * (BAKRON_DEFER unset), the first solve of that shape on the handle runs
+ * both plans twice each, times them with events on `stream` (one host
+ * synchronisation), keeps the faster for the handle and returns the outputs
+ * of its last run.  On the legacy default stream, which
  * synchronises implicitly with such streams, and while `stream` is being
  * captured into a graph, everything runs on `stream`.  Unless
  * BAKRON_DEFER=0, the first solve planned on a device creates the two

@@ -64,6 +64,10 @@ struct bakron_factors {
     // to every tile in the same order, so their results are identical.
     bk::Plan plan[2];
     int last_plan = 0;
+    // with the cost model's choice (BAKRON_DEFER unset) a two-stream plan is
+    // timed against the one-stream plan on the first solve of its shape
+    int tune = 0;
+    hipEvent_t tev[2] = {nullptr, nullptr};
     const int4* items = nullptr;    // device copy, owned by the process-wide plan cache
     // measurement hook: per timed launch (enqueue order) its class and work
     int prof = 0;
@@ -456,6 +460,8 @@ extern "C" void bakron_factors_free(bakron_factors* f) {
     if (f->ad_mem) hipFree(f->ad_mem);
     if (f->gq_mem) hipFree(f->gq_mem);
     // f->side, f->main and f->items belong to the process-wide plan cache
+    for (hipEvent_t ev : f->tev)
+        if (ev) hipEventDestroy(ev);
     if (f->ev_fork) hipEventDestroy(f->ev_fork);
     if (f->ev_join) hipEventDestroy(f->ev_join);
     for (hipEvent_t ev : f->ev_rel) hipEventDestroy(ev);
@@ -684,6 +690,7 @@ static bakron_status plan_with_side_stream(bakron_factors* f, int mt, int nt) {
     f->main = pe->main;
     f->side = pe->side;
     f->side_cu_lo = pe->plan[1].side.empty() ? -1 : pe->plan[1].side_cu_lo;
+    f->tune = defer == 2 && !pe->plan[1].side.empty();
     if (pe->plan[1].side.empty()) return BAKRON_OK;
     auto grow = [](std::vector<hipEvent_t>& v, size_t need) {
         while (v.size() < need) {
@@ -845,6 +852,7 @@ static bakron_status solve_impl(const float* W, int64_t m, int64_t n, const bakr
     bakron_status st = check_solve_args(f, "bakron_solve", W, m, n, q, codes, V);
     if (st != BAKRON_OK) return st;
     if (f->b_ident && f->gptq) return solve_gptq(f, W, m, n, q, codes, V, pre, stream);
+    const bool fresh = !(f->ws_m == m && f->ws_n == n && f->ws_mem);   // first solve of this shape
     st = ensure_workspace(f, m, n);
     if (st != BAKRON_OK) return st;
     const int mt = (int)cdiv(m, bk::TS), nt = (int)cdiv(n, bk::TS);
@@ -867,7 +875,16 @@ static bakron_status solve_impl(const float* W, int64_t m, int64_t n, const bakr
     // two-stream fork is not captured)
     hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
     if (!legacy && hipStreamIsCapturing(stream, &cap) != hipSuccess) cap = hipStreamCaptureStatusNone;
-    const int pi = (!legacy && cap == hipStreamCaptureStatusNone && !f->plan[1].side.empty()) ? 1 : 0;
+    int pi = (!legacy && cap == hipStreamCaptureStatusNone && !f->plan[1].side.empty()) ? 1 : 0;
+    // The first solve of a shape for which the cost model chose the two-stream
+    // plan runs both plans (twice each, the second runs timed, one host
+    // synchronisation) and keeps the faster one for the handle: the two-stream
+    // time depends on what the process did on other streams before (up to 25%
+    // slower on MI355X), the one-stream time does not.  Both plans write the
+    // same outputs.  The first solve of a shape allocates anyway, so later
+    // calls keep their no-allocation, no-synchronisation contract.
+    const bool tune = fresh && f->tune && pi == 1 && !f->prof;
+    if (fresh) f->tune = 0;
     f->last_plan = pi;
     hipEvent_t* tim = nullptr;
     f->prof_valid = 0;
@@ -881,25 +898,51 @@ static bakron_status solve_impl(const float* W, int64_t m, int64_t n, const bakr
         }
         tim = f->tim.data();
     }
-    // with side ops the main ops run on the handle's non-blocking stream,
-    // forked from and joined back into the caller's stream
-    const bool fork = pi == 1;
-    hipStream_t ms = fork ? f->main : stream;
+    // one solve with plan `plan`; with side ops the main ops run on the
+    // handle's CU-restricted main stream, forked from and joined back into
+    // the caller's stream
+    auto launch = [&](int plan) -> hipError_t {
+        const bool fork = plan == 1;
+        hipStream_t ms = fork ? f->main : stream;
+        hipError_t e = hipSuccess;
+        // poisoning spares the last two words (the sticky status and the scale flag)
+        if (f->poison) e = bk::fill_words(stream, f->ws_mem, (int64_t)(f->ws_bytes / 4) - 2, 0xFFFFFFFFu);
+        if (fork && e == hipSuccess) {
+            e = hipEventRecord(f->ev_fork, stream);
+            if (e == hipSuccess) e = hipStreamWaitEvent(ms, f->ev_fork, 0);
+        }
+        if (e == hipSuccess)
+            e = bk::run_plan(ms, f->side, f->plan[plan], W, m, n, mt, nt, f->ws, f->LA, f->LB,
+                             f->b_ident, qa, codes, V, pre, f->knear, spin_limit, f->items,
+                             plan == pi ? tim : nullptr, f->ev_rel.data(), f->ev_side.data());
+        if (fork && e == hipSuccess) {
+            e = hipEventRecord(f->ev_join, ms);
+            if (e == hipSuccess) e = hipStreamWaitEvent(stream, f->ev_join, 0);
+        }
+        return e;
+    };
     hipError_t e = hipSuccess;
-    // poisoning spares the last two words (the sticky status and the scale flag)
-    if (f->poison) e = bk::fill_words(stream, f->ws_mem, (int64_t)(f->ws_bytes / 4) - 2, 0xFFFFFFFFu);
-    if (fork && e == hipSuccess) {
-        e = hipEventRecord(f->ev_fork, stream);
-        if (e == hipSuccess) e = hipStreamWaitEvent(ms, f->ev_fork, 0);
+    if (tune) {
+        for (hipEvent_t& ev : f->tev)
+            if (!ev && e == hipSuccess) e = hipEventCreate(&ev);
+        float t[2] = {0.0f, 0.0f};
+        for (int rep = 0; rep < 2 && e == hipSuccess; ++rep)
+            for (int plan = 0; plan <= 1 && e == hipSuccess; ++plan) {
+                e = hipEventRecord(f->tev[0], stream);
+                if (e == hipSuccess) e = launch(plan);
+                if (e == hipSuccess) e = hipEventRecord(f->tev[1], stream);
+                if (e == hipSuccess) e = hipEventSynchronize(f->tev[1]);
+                if (e == hipSuccess && rep == 1) e = hipEventElapsedTime(&t[plan], f->tev[0], f->tev[1]);
+            }
+        if (e != hipSuccess) return hip_fail(&f->err, e, "bakron_solve: timing the plans");
+        if (t[0] <= t[1]) {   // one stream from now on for this handle and shape
+            f->plan[1] = bk::Plan{};
+            pi = 0;
+        }
+        f->last_plan = pi;
+        return BAKRON_OK;   // the outputs of the last run (two streams) are the solve's
     }
-    if (e == hipSuccess)
-        e = bk::run_plan(ms, f->side, f->plan[pi], W, m, n, mt, nt, f->ws, f->LA, f->LB, f->b_ident,
-                         qa, codes, V, pre, f->knear, spin_limit, f->items, tim,
-                         f->ev_rel.data(), f->ev_side.data());
-    if (fork && e == hipSuccess) {
-        e = hipEventRecord(f->ev_join, ms);
-        if (e == hipSuccess) e = hipStreamWaitEvent(stream, f->ev_join, 0);
-    }
+    e = launch(pi);
     if (e != hipSuccess) return hip_fail(&f->err, e, "bakron_solve: launch");
     f->prof_valid = f->prof;
     return BAKRON_OK;
