@@ -794,6 +794,8 @@ def main():
     # the segment launches carry the sequential chain: per tile anti-diagonal
     n_diag = (m + 31) // 32 + (n + 31) // 32 - 1
     seg["us_per_tile_diagonal"] = seg["ms_per_step"] * 1e3 / n_diag
+    # and per sequential step of the method (one element anti-diagonal, m + n - 1)
+    seg["us_per_element_diagonal"] = seg["ms_per_step"] * 1e3 / (m + n - 1)
     # wavefront bandwidth: HBM bytes per launch (rocprofv3 counters, while the
     # kernel source is unchanged) over the live average launch duration
     seg_traffic = measured_traffic("k_seg", cfg.name)

@@ -172,38 +172,48 @@ __global__ __launch_bounds__(NB) void k_inv_lower_blocks(const double* __restric
 // MFMA (v_mfma_f64_16x16x4f64: lane l supplies A[l % 16][l / 16] and
 // B[l / 16][l % 16] of a k-step; register r of lane l holds
 // D[l / 16 + 4 r][l % 16]).
-// op(B) = B (K x N, ldb) or B^T (B is N x K, ldb).  lower_only skips output
-// blocks lying entirely above the diagonal (row index < col index) of C.
+// op(B) = B (K x N, ldb) or B^T (B is N x K, ldb).  lower_only skips the
+// 64 x 64 blocks of C lying entirely above the diagonal (block column index >
+// block row index): they are neither computed nor written.
 // tri: bit 0 = A is lower triangular (A[i][k] = 0 for k > i), bit 1 = op(B)
 // is lower triangular (op(B)[k][j] = 0 for k < j); the K loop of a block then
 // skips the chunks that only meet those zeros.
-// One workgroup per 64 x 64 block of C, 4 waves of 2 x 2 MFMA blocks; K in
-// chunks of 16 staged through double-buffered LDS as [k][row] / [k][col],
-// the next chunk loaded into registers while the current one is multiplied.
+// One workgroup per GT x GT block of C (GT = 64 or 128): GT / 16 waves, wave
+// (wm, wn) computing rows 32 wm .. 32 wm + 31 and GT / 2 columns from
+// wn * GT / 2 as 2 x (GT / 32) MFMA blocks.  K in chunks of 16 staged through
+// double-buffered LDS as [k][row] / [k][col], the next chunk loaded into
+// registers while the current one is multiplied.  The 128 x 128 block stages
+// half as many bytes per flop.  Every entry of C sees the same MFMA sequence
+// over the same K chunks in both block sizes, except that under `tri` a
+// larger block may visit extra chunks whose products are exact zeros; those
+// can only change the sign of an entry that is exactly zero, so zeros are
+// stored as +0 and both block sizes give the same bits.
 typedef double f64x4 __attribute__((ext_vector_type(4)));
-constexpr int GB = 64, GK = 16, GPAD = GB + 2;
-__global__ __launch_bounds__(256) void k_gemm64(int64_t M, int64_t N, int64_t K, double alpha,
-                                                const double* __restrict__ A, int64_t lda,
-                                                const double* __restrict__ B, int64_t ldb,
-                                                int transB, double beta, double* __restrict__ C,
-                                                int64_t ldc, int lower_only, int tri,
-                                                const int* __restrict__ fail) {
+constexpr int GK = 16;
+template <int GT>
+__global__ __launch_bounds__(4 * GT) void k_gemm(int64_t M, int64_t N, int64_t K, double alpha,
+                                                 const double* __restrict__ A, int64_t lda,
+                                                 const double* __restrict__ B, int64_t ldb,
+                                                 int transB, double beta, double* __restrict__ C,
+                                                 int64_t ldc, int lower_only, int tri,
+                                                 const int* __restrict__ fail) {
+    constexpr int PAD = GT + 2, YB = GT / 32;
     if (*fail) return;
-    const int64_t r0 = (int64_t)blockIdx.y * GB, c0 = (int64_t)blockIdx.x * GB;
-    if (lower_only && c0 > r0 + GB - 1) return;
+    const int64_t r0 = (int64_t)blockIdx.y * GT, c0 = (int64_t)blockIdx.x * GT;
+    if (lower_only && c0 > r0 + GT - 1) return;
     // K range that can hold nonzero products for this block (GK-aligned start)
     const int64_t kbeg = (tri & 2) ? (c0 < K ? c0 / GK * GK : K) : 0;
-    const int64_t kend = (tri & 1) ? (r0 + GB < K ? r0 + GB : K) : K;
-    __shared__ double As[2][GK][GPAD];
-    __shared__ double Bs[2][GK][GPAD];
+    const int64_t kend = (tri & 1) ? (r0 + GT < K ? r0 + GT : K) : K;
+    __shared__ double As[2][GK][PAD];
+    __shared__ double Bs[2][GK][PAD];
     const int t = threadIdx.x;
     const int wv = t >> 6, l = t & 63;
     const int wm = wv >> 1, wn = wv & 1;
     const int li = l & 15, lk = l >> 4;
     // staging: A rows (and B^T rows) by t >> 2, k quarter 4 (t & 3); B rows
-    // (k) by t >> 4, column quarter 4 (t & 15)
+    // (k) by t / (GT / 4), column quarter 4 (t % (GT / 4))
     const int ar = t >> 2, aq = 4 * (t & 3);
-    const int bk = t >> 4, bq = 4 * (t & 15);
+    const int bk = t / (GT / 4), bq = 4 * (t % (GT / 4));
     double ra[4], rb[4];
     auto load = [&](int64_t k0) {
 #pragma unroll
@@ -236,11 +246,11 @@ __global__ __launch_bounds__(256) void k_gemm64(int64_t M, int64_t N, int64_t K,
             for (int u = 0; u < 4; ++u) Bs[sb][aq + u][ar] = rb[u];
         }
     };
-    f64x4 acc[2][2];
+    f64x4 acc[2][YB];
 #pragma unroll
     for (int x = 0; x < 2; ++x)
 #pragma unroll
-        for (int y = 0; y < 2; ++y) acc[x][y] = f64x4{0.0, 0.0, 0.0, 0.0};
+        for (int y = 0; y < YB; ++y) acc[x][y] = f64x4{0.0, 0.0, 0.0, 0.0};
     const int64_t nch = kend > kbeg ? (kend - kbeg + GK - 1) / GK : 0;
     if (nch > 0) {
         load(kbeg);
@@ -254,15 +264,15 @@ __global__ __launch_bounds__(256) void k_gemm64(int64_t M, int64_t N, int64_t K,
 #pragma unroll
         for (int kk = 0; kk < GK / 4; ++kk) {
             const int kr = 4 * kk + lk;
-            double a[2], b2[2];
+            double a[2], b2[YB];
 #pragma unroll
             for (int x = 0; x < 2; ++x) a[x] = As[sb][kr][wm * 32 + x * 16 + li];
 #pragma unroll
-            for (int y = 0; y < 2; ++y) b2[y] = Bs[sb][kr][wn * 32 + y * 16 + li];
+            for (int y = 0; y < YB; ++y) b2[y] = Bs[sb][kr][wn * (GT / 2) + y * 16 + li];
 #pragma unroll
             for (int x = 0; x < 2; ++x)
 #pragma unroll
-                for (int y = 0; y < 2; ++y)
+                for (int y = 0; y < YB; ++y)
                     acc[x][y] = __builtin_amdgcn_mfma_f64_16x16x4f64(a[x], b2[y], acc[x][y], 0, 0, 0);
         }
         if (more) store(sb ^ 1);
@@ -271,15 +281,17 @@ __global__ __launch_bounds__(256) void k_gemm64(int64_t M, int64_t N, int64_t K,
 #pragma unroll
     for (int x = 0; x < 2; ++x)
 #pragma unroll
-        for (int y = 0; y < 2; ++y) {
-            const int64_t gc = c0 + wn * 32 + y * 16 + li;
+        for (int y = 0; y < YB; ++y) {
+            const int64_t gc = c0 + wn * (GT / 2) + y * 16 + li;
             if (gc >= N) continue;
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
                 const int64_t gr = r0 + wm * 32 + x * 16 + lk + 4 * r;
                 if (gr >= M) continue;
+                if (lower_only && (gc >> 6) > (gr >> 6)) continue;   // a 64 x 64 block above the diagonal
                 double* cp = C + gr * ldc + gc;
-                *cp = (beta == 0.0) ? alpha * acc[x][y][r] : alpha * acc[x][y][r] + beta * (*cp);
+                const double v = (beta == 0.0) ? alpha * acc[x][y][r] : alpha * acc[x][y][r] + beta * (*cp);
+                *cp = v + 0.0;   // -0 -> +0: zeros do not depend on which chunks were visited
             }
         }
 }
@@ -360,14 +372,32 @@ static inline unsigned grid1d(int64_t total, int threads = 256) {
     return (unsigned)g;
 }
 
-static hipError_t gemm64(hipStream_t s, int64_t M, int64_t N, int64_t K, double alpha,
+// 128 x 128 blocks when there are enough of them to fill the chip twice
+// over (counting only blocks on or below the diagonal for lower_only), else
+// 64 x 64 blocks.
+#ifndef GEMM128_MIN_BLOCKS
+#define GEMM128_MIN_BLOCKS 512
+#endif
+static hipError_t gemm_f64(hipStream_t s, int64_t M, int64_t N, int64_t K, double alpha,
                          const double* A, int64_t lda, const double* B, int64_t ldb, int transB,
                          double beta, double* C, int64_t ldc, int lower, const int* fail,
                          int tri = 0) {
     if (M <= 0 || N <= 0) return hipSuccess;
-    dim3 grid((unsigned)((N + GB - 1) / GB), (unsigned)((M + GB - 1) / GB));
-    hipLaunchKernelGGL(k_gemm64, grid, dim3(256), 0, s, M, N, K, alpha, A, lda, B, ldb, transB,
-                       beta, C, ldc, lower, tri, fail);
+    const int64_t bm = (M + 127) / 128, bn = (N + 127) / 128;
+    int64_t active = bm * bn;
+    if (lower) {   // blocks with block column <= block row
+        active = 0;
+        for (int64_t i = 0; i < bm; ++i) active += (i + 1 < bn ? i + 1 : bn);
+    }
+    if (active >= GEMM128_MIN_BLOCKS) {
+        dim3 grid((unsigned)bn, (unsigned)bm);
+        hipLaunchKernelGGL(k_gemm<128>, grid, dim3(512), 0, s, M, N, K, alpha, A, lda, B, ldb,
+                           transB, beta, C, ldc, lower, tri, fail);
+    } else {
+        dim3 grid((unsigned)((N + 63) / 64), (unsigned)((M + 63) / 64));
+        hipLaunchKernelGGL(k_gemm<64>, grid, dim3(256), 0, s, M, N, K, alpha, A, lda, B, ldb,
+                           transB, beta, C, ldc, lower, tri, fail);
+    }
     return hipGetLastError();
 }
 
@@ -385,11 +415,11 @@ static hipError_t trtri_rec(hipStream_t s, const double* C, double* Ninv, int64_
     if (e != hipSuccess) return e;
     const int64_t n2 = sz - h;
     // T (n2 x h) = C21 * N11 (N11 lower triangular)
-    e = gemm64(s, n2, h, h, 1.0, C + (off + h) * ld + off, ld, Ninv + off * ld + off, ld, 0, 0.0, T,
+    e = gemm_f64(s, n2, h, h, 1.0, C + (off + h) * ld + off, ld, Ninv + off * ld + off, ld, 0, 0.0, T,
                h, 0, fail, 2);
     if (e != hipSuccess) return e;
     // N21 = -N22 * T (N22 lower triangular)
-    return gemm64(s, n2, h, n2, -1.0, Ninv + (off + h) * ld + (off + h), ld, T, h, 0, 0.0,
+    return gemm_f64(s, n2, h, n2, -1.0, Ninv + (off + h) * ld + (off + h), ld, T, h, 0, 0.0,
                   Ninv + (off + h) * ld + off, ld, 0, fail, 1);
 }
 
@@ -418,7 +448,7 @@ hipError_t factor_one(hipStream_t s, const float* X, int64_t d, double lam, doub
                 hipLaunchKernelGGL(k_trsm_panel, dim3((unsigned)((rest + 255) / 256)), dim3(256), 0,
                                    s, Z, d, k0, b, rest, fail);
                 // the panel's remaining columns: Z[k0+b:, k0+b:pend] -= P P[k0+b:pend]^T
-                e = gemm64(s, rest, pend - k0 - b, b, -1.0, Z + (k0 + b) * d + k0, d,
+                e = gemm_f64(s, rest, pend - k0 - b, b, -1.0, Z + (k0 + b) * d + k0, d,
                            Z + (k0 + b) * d + k0, d, 1, 1.0, Z + (k0 + b) * d + (k0 + b), d, 1, fail);
                 if (e != hipSuccess) return e;
             }
@@ -426,7 +456,7 @@ hipError_t factor_one(hipStream_t s, const float* X, int64_t d, double lam, doub
         const int64_t rest = d - pend;
         if (rest > 0) {
             // trailing update Z22 -= P P^T over the whole panel (lower blocks)
-            e = gemm64(s, rest, rest, pend - p0, -1.0, Z + pend * d + p0, d, Z + pend * d + p0, d, 1,
+            e = gemm_f64(s, rest, rest, pend - p0, -1.0, Z + pend * d + p0, d, Z + pend * d + p0, d, 1,
                        1.0, Z + pend * d + pend, d, 1, fail);
             if (e != hipSuccess) return e;
         }
