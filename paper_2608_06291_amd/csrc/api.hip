@@ -18,9 +18,9 @@
 #include <vector>
 
 namespace bk {
-hipError_t factor_one(hipStream_t s, const float* X, int64_t d, double lam, double* Z, double* Ninv,
-                      double* T, double* mean, int* fail, int64_t* fail_pivot, float* packed,
-                      int64_t nt);
+hipError_t factor_one(hipStream_t s, hipStream_t s2, hipEvent_t ev_panel, hipEvent_t ev_rest,
+                      const float* X, int64_t d, double lam, double* Z, double* Ninv, double* T,
+                      double* mean, int* fail, int64_t* fail_pivot, float* packed, int64_t nt);
 hipError_t pack_identity(hipStream_t s, int64_t nt, float* packed);
 hipError_t unpack_factor(hipStream_t s, const float* packed, int64_t d, float* dst);
 
@@ -353,13 +353,16 @@ extern "C" bakron_status bakron_factor(const float* A, int64_t n, const float* B
 
     // A and B are factored concurrently (their block steps are latency-bound):
     // B on a second, non-blocking stream forked from and joined back into
-    // `stream`, each with its own scratch
+    // `stream`, each with its own scratch; each factorisation has one more
+    // stream for the trailing updates it runs one panel ahead of
     const int64_t ntA = cdiv(n, bk::TS);
     double *Z[2] = {nullptr, nullptr}, *Ninv[2] = {nullptr, nullptr}, *T[2] = {nullptr, nullptr};
     double* scal = nullptr;
     int* flags = nullptr;
     hipStream_t sB = nullptr;
     hipEvent_t ev[2] = {nullptr, nullptr};
+    hipStream_t s2[2] = {nullptr, nullptr};
+    hipEvent_t evp[2] = {nullptr, nullptr}, evr[2] = {nullptr, nullptr};
     bakron_status st = BAKRON_OK;
     hipError_t e = hipSuccess;
     auto cleanup = [&]() {
@@ -368,6 +371,9 @@ extern "C" bakron_status bakron_factor(const float* A, int64_t n, const float* B
             if (Ninv[k]) hipFree(Ninv[k]);
             if (T[k]) hipFree(T[k]);
             if (ev[k]) hipEventDestroy(ev[k]);
+            if (evp[k]) hipEventDestroy(evp[k]);
+            if (evr[k]) hipEventDestroy(evr[k]);
+            if (s2[k]) hipStreamDestroy(s2[k]);
         }
         if (scal) hipFree(scal);
         if (flags) hipFree(flags);
@@ -389,6 +395,11 @@ extern "C" bakron_status bakron_factor(const float* A, int64_t n, const float* B
         return st;
     }
     e = hipMemsetAsync(flags, 0, 8 * sizeof(int64_t), stream);
+    for (int k = 0; k < (B ? 2 : 1) && e == hipSuccess; ++k) {
+        e = hipStreamCreateWithFlags(&s2[k], hipStreamNonBlocking);
+        if (e == hipSuccess) e = hipEventCreateWithFlags(&evp[k], hipEventDisableTiming);
+        if (e == hipSuccess) e = hipEventCreateWithFlags(&evr[k], hipEventDisableTiming);
+    }
     if (e == hipSuccess && B) {
         e = hipStreamCreateWithFlags(&sB, hipStreamNonBlocking);
         if (e == hipSuccess) e = hipEventCreateWithFlags(&ev[0], hipEventDisableTiming);
@@ -403,12 +414,12 @@ extern "C" bakron_status bakron_factor(const float* A, int64_t n, const float* B
         f->LB_tiles = mtB;
         e = hipMalloc(&f->LB, sizeof(float) * (size_t)(mtB * (mtB + 1) / 2) * bk::TILE_ELEMS);
         if (e == hipSuccess)
-            e = bk::factor_one(sB, B, m, (double)damp, Z[1], Ninv[1], T[1], scal + 1, flags + 1,
-                               reinterpret_cast<int64_t*>(flags) + 3, f->LB, mtB);
+            e = bk::factor_one(sB, s2[1], evp[1], evr[1], B, m, (double)damp, Z[1], Ninv[1], T[1],
+                               scal + 1, flags + 1, reinterpret_cast<int64_t*>(flags) + 3, f->LB, mtB);
     }
     if (e == hipSuccess)
-        e = bk::factor_one(stream, A, n, (double)damp, Z[0], Ninv[0], T[0], scal, flags,
-                           reinterpret_cast<int64_t*>(flags) + 2, f->LA, ntA);
+        e = bk::factor_one(stream, s2[0], evp[0], evr[0], A, n, (double)damp, Z[0], Ninv[0], T[0],
+                           scal, flags, reinterpret_cast<int64_t*>(flags) + 2, f->LA, ntA);
     if (e == hipSuccess && B) {
         e = hipEventRecord(ev[1], sB);
         if (e == hipSuccess) e = hipStreamWaitEvent(stream, ev[1], 0);
@@ -416,6 +427,8 @@ extern "C" bakron_status bakron_factor(const float* A, int64_t n, const float* B
     if (e != hipSuccess) {
         st = hip_fail(&g_last_error, e, "bakron_factor: launch");
         if (sB) (void)hipStreamSynchronize(sB);
+        for (hipStream_t x : s2)
+            if (x) (void)hipStreamSynchronize(x);
         cleanup();
         bakron_factors_free(f);
         return st;

@@ -199,7 +199,21 @@ __global__ __launch_bounds__(4 * GT) void k_gemm(int64_t M, int64_t N, int64_t K
                                                  const int* __restrict__ fail) {
     constexpr int PAD = GT + 2, YB = GT / 32;
     if (*fail) return;
-    const int64_t r0 = (int64_t)blockIdx.y * GT, c0 = (int64_t)blockIdx.x * GT;
+    // block order: under tri the heaviest K ranges first, so that the longest
+    // blocks do not start last (bit 0: the range grows with the block row, so
+    // rows run bottom-up; bit 1: it shrinks with the block column, so blocks
+    // run column by column from the left)
+    const int64_t nbx = gridDim.x, nby = gridDim.y;
+    const int64_t bid = (int64_t)blockIdx.y * nbx + blockIdx.x;
+    int64_t bx = blockIdx.x, by = blockIdx.y;
+    if (tri & 1) {
+        by = nby - 1 - bid / nbx;
+        bx = bid % nbx;
+    } else if (tri & 2) {
+        bx = bid / nby;
+        by = bid % nby;
+    }
+    const int64_t r0 = by * GT, c0 = bx * GT;
     if (lower_only && c0 > r0 + GT - 1) return;
     // K range that can hold nonzero products for this block (GK-aligned start)
     const int64_t kbeg = (tri & 2) ? (c0 < K ? c0 / GK * GK : K) : 0;
@@ -424,10 +438,12 @@ static hipError_t trtri_rec(hipStream_t s, const double* C, double* Ninv, int64_
 }
 
 // Factor one matrix.  Z, Ninv: d*d doubles; T: d*d/4 + d*NB doubles;
-// flag: 1 int + 1 int64 (fail, pivot) zeroed by the caller.
-hipError_t factor_one(hipStream_t s, const float* X, int64_t d, double lam, double* Z, double* Ninv,
-                      double* T, double* mean, int* fail, int64_t* fail_pivot, float* packed,
-                      int64_t nt) {
+// flag: 1 int + 1 int64 (fail, pivot) zeroed by the caller.  With s2 (and
+// its two events) the Cholesky looks one panel ahead; s2's work is ordered
+// before everything enqueued on s after the call.
+hipError_t factor_one(hipStream_t s, hipStream_t s2, hipEvent_t ev_panel, hipEvent_t ev_rest,
+                      const float* X, int64_t d, double lam, double* Z, double* Ninv, double* T,
+                      double* mean, int* fail, int64_t* fail_pivot, float* packed, int64_t nt) {
     hipLaunchKernelGGL(k_diag_mean, dim3(1), dim3(256), 0, s, X, d, mean);
     hipLaunchKernelGGL(k_flip_damp, dim3(grid1d(d * d)), dim3(256), 0, s, X, d, mean, lam, Z);
     hipError_t e = hipGetLastError();
@@ -436,7 +452,13 @@ hipError_t factor_one(hipStream_t s, const float* X, int64_t d, double lam, doub
     // in NB-column steps (diagonal block, substitution for every row below,
     // update of the panel's remaining columns), then one rank-NB2 update of
     // the trailing matrix, which reads and writes it NB2 / NB times less
-    // often than rank-NB updates would.
+    // often than rank-NB updates would.  With s2 the trailing update of a
+    // panel is split: the columns of the next panel on s, the rest on s2,
+    // where it overlaps the next panel's factorisation (a chain of small,
+    // latency-bound launches).  The rest update of panel p writes only
+    // columns that panel p + 1 does not touch, and the next-panel update of
+    // panel p + 1 waits for it, so every entry receives the same updates in
+    // the same order either way.
     for (int64_t p0 = 0; p0 < d; p0 += NB2) {
         const int64_t pend = (d - p0) < NB2 ? d : p0 + NB2;
         for (int64_t k0 = p0; k0 < pend; k0 += NB) {
@@ -449,17 +471,29 @@ hipError_t factor_one(hipStream_t s, const float* X, int64_t d, double lam, doub
                                    s, Z, d, k0, b, rest, fail);
                 // the panel's remaining columns: Z[k0+b:, k0+b:pend] -= P P[k0+b:pend]^T
                 e = gemm_f64(s, rest, pend - k0 - b, b, -1.0, Z + (k0 + b) * d + k0, d,
-                           Z + (k0 + b) * d + k0, d, 1, 1.0, Z + (k0 + b) * d + (k0 + b), d, 1, fail);
+                             Z + (k0 + b) * d + k0, d, 1, 1.0, Z + (k0 + b) * d + (k0 + b), d, 1, fail);
                 if (e != hipSuccess) return e;
             }
         }
         const int64_t rest = d - pend;
-        if (rest > 0) {
-            // trailing update Z22 -= P P^T over the whole panel (lower blocks)
-            e = gemm_f64(s, rest, rest, pend - p0, -1.0, Z + pend * d + p0, d, Z + pend * d + p0, d, 1,
-                       1.0, Z + pend * d + pend, d, 1, fail);
+        if (rest <= 0) continue;
+        const double* P = Z + pend * d + p0;   // the factored panel's rows below it
+        const int64_t kp = pend - p0;
+        // split point: the end of the next panel (no split without s2)
+        const int64_t nend = (s2 && d - pend > NB2) ? pend + NB2 : d;
+        if (nend < d) {   // Z[nend:, nend:] -= P P^T on s2, after this panel
+            if ((e = hipEventRecord(ev_panel, s)) != hipSuccess) return e;
+            if ((e = hipStreamWaitEvent(s2, ev_panel, 0)) != hipSuccess) return e;
+            e = gemm_f64(s2, d - nend, d - nend, kp, -1.0, P + (nend - pend) * d, d,
+                         P + (nend - pend) * d, d, 1, 1.0, Z + nend * d + nend, d, 1, fail);
             if (e != hipSuccess) return e;
         }
+        // the previous panel's rest update also wrote these columns
+        if (s2 && p0 > 0 && (e = hipStreamWaitEvent(s, ev_rest, 0)) != hipSuccess) return e;
+        // Z[pend:, pend:nend] -= P P[pend:nend]^T on s
+        e = gemm_f64(s, rest, nend - pend, kp, -1.0, P, d, P, d, 1, 1.0, Z + pend * d + pend, d, 1, fail);
+        if (e != hipSuccess) return e;
+        if (nend < d && (e = hipEventRecord(ev_rest, s2)) != hipSuccess) return e;
     }
     // Ninv = C^-1 (lower); upper part must be zero for the recursive GEMMs
     e = hipMemsetAsync(Ninv, 0, sizeof(double) * d * d, s);

@@ -130,7 +130,7 @@ int main() {
     return fails;
 }
 namespace bk {
-hipError_t factor_one(hipStream_t, const float*, int64_t, double, double*, double*, double*, double*, int*, int64_t*, float*, int64_t) { return hipSuccess; }
+hipError_t factor_one(hipStream_t, hipStream_t, hipEvent_t, hipEvent_t, const float*, int64_t, double, double*, double*, double*, double*, int*, int64_t*, float*, int64_t) { return hipSuccess; }
 hipError_t pack_identity(hipStream_t, int64_t, float*) { return hipSuccess; }
 hipError_t unpack_factor(hipStream_t, const float*, int64_t, float*) { return hipSuccess; }
 int plan_timed_launches(const Plan&) { return 0; }
