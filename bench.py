@@ -505,21 +505,26 @@ def quant_bench(steps: int):
 
 
 def factorise_bench(dims, steps: int):
-    """bakron_factor alone on two d x d factors (damping, reverse Cholesky,
-    triangular inverse and packing; A and B concurrently), inputs
-    the AR(1) Toeplitz matrices rho^|i-j| (rho 0.5 / 0.2) resident in HBM.
-    Counted fp64 work 4 d^3 / 3 (d^3 / 3 for each Cholesky and each inverse).
-    One JSON line per d."""
+    """bakron_factor alone on factor pairs (damping, reverse Cholesky,
+    triangular inverse and packing; A and B concurrently), inputs the AR(1)
+    Toeplitz matrices rho^|i-j| (rho 0.5 for A, 0.2 for B) resident in HBM.
+    Each entry of `dims` is d (A and B both d x d) or n:m (A n x n, B m x m,
+    as in a layer's factor pair).  Counted fp64 work 2 d^3 / 3 per factor
+    (d^3 / 3 for its Cholesky and d^3 / 3 for its inverse).  One JSON line per
+    entry, with the median of `steps` calls after one warm-up call."""
     import torch
     import paper_2608_06291_amd as pk
     dev = torch.device("cuda:0")
     stream = torch.cuda.Stream(dev)
     torch.cuda.set_stream(stream)
-    for d in dims:
+
+    def ar1(d, rho):
         i = torch.arange(d, device=dev, dtype=torch.float32)
-        A = 0.5 ** (i[:, None] - i[None, :]).abs()
-        B = 0.2 ** (i[:, None] - i[None, :]).abs()
-        del i
+        return rho ** (i[:, None] - i[None, :]).abs()
+
+    for spec in dims:
+        n, m = (int(x) for x in spec.split(":")) if ":" in spec else (int(spec), int(spec))
+        A, B = ar1(n, 0.5), ar1(m, 0.2)
         pk.factor(A, B, 0.01).close()            # warm-up: scratch allocation, clocks
         torch.cuda.synchronize()
         ts = []
@@ -530,10 +535,10 @@ def factorise_bench(dims, steps: int):
             ts.append((time.perf_counter() - t0) * 1e3)
             f.close()
         ms = sorted(ts)[len(ts) // 2]
-        flops = 4.0 * d ** 3 / 3.0
+        flops = 2.0 * (n ** 3 + m ** 3) / 3.0
         tf = flops / (ms * 1e-3) / 1e12
-        print(json.dumps({"metric": "bakron_factor ms (A and B, d x d each, concurrently)",
-                          "value": ms, "unit": "ms", "higher_is_better": False, "d": d,
+        print(json.dumps({"metric": "bakron_factor ms (A n x n and B m x m, concurrently)",
+                          "value": ms, "unit": "ms", "higher_is_better": False, "n": n, "m": m,
                           "steps": steps, "counted_fp64_tflop": flops / 1e12,
                           "fp64_tflops": tf, "frac_fp64_mfma_peak": tf / PEAK_FP64_MFMA,
                           "data": "synthetic"}), flush=True)
@@ -648,9 +653,9 @@ def main():
     ap.add_argument("--quant", action="store_true",
                     help="only time the quantiser variants and the MSE scale search on the "
                          "4096 x 4096 layer and exit")
-    ap.add_argument("--factorise", default=None, metavar="d[,d...]",
-                    help="time bakron_factor alone on d x d factor pairs (damping, reverse "
-                         "Cholesky, triangular inverse)")
+    ap.add_argument("--factorise", default=None, metavar="d|n:m[,...]",
+                    help="time bakron_factor alone on factor pairs, d x d both or A n x n and "
+                         "B m x m (damping, reverse Cholesky, triangular inverse)")
     ap.add_argument("--flow", default=None, metavar="L,d,N[,style]",
                     help="only run the recursive backprop flow (Sec. 5) over L layers of width d "
                          "with N samples (style kfac or shampooK) and exit")
@@ -677,7 +682,7 @@ def main():
         return
 
     if args.factorise:
-        factorise_bench([int(x) for x in args.factorise.split(",")], max(args.steps, 1))
+        factorise_bench(args.factorise.split(","), max(args.steps, 1))
         return
     if args.flow:
         parts = args.flow.split(",")
