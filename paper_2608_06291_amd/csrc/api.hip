@@ -354,7 +354,7 @@ extern "C" bakron_status bakron_factor(const float* A, int64_t n, const float* B
     // A and B are factored concurrently (their block steps are latency-bound):
     // B on a second, non-blocking stream forked from and joined back into
     // `stream`, each with its own scratch; each factorisation has one more
-    // stream for the trailing updates it runs one panel ahead of
+    // stream for the trailing updates it runs one panel ahead of (d >= 8192)
     const int64_t ntA = cdiv(n, bk::TS);
     double *Z[2] = {nullptr, nullptr}, *Ninv[2] = {nullptr, nullptr}, *T[2] = {nullptr, nullptr};
     double* scal = nullptr;
@@ -395,7 +395,10 @@ extern "C" bakron_status bakron_factor(const float* A, int64_t n, const float* B
         return st;
     }
     e = hipMemsetAsync(flags, 0, 8 * sizeof(int64_t), stream);
+    // the look-ahead pays only where a trailing update outlasts the next
+    // panel's chain of small launches; smaller factors create no stream
     for (int k = 0; k < (B ? 2 : 1) && e == hipSuccess; ++k) {
+        if ((k == 0 ? n : m) < 8192) continue;
         e = hipStreamCreateWithFlags(&s2[k], hipStreamNonBlocking);
         if (e == hipSuccess) e = hipEventCreateWithFlags(&evp[k], hipEventDisableTiming);
         if (e == hipSuccess) e = hipEventCreateWithFlags(&evr[k], hipEventDisableTiming);
