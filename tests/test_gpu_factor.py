@@ -66,6 +66,35 @@ def test_factor_ar1_closed_form():
     assert np.abs(L - ref).max() <= 1e-6
 
 
+def test_factor_ar1_closed_form_large():
+    """The same closed form at sizes that take the 128 x 128 fp64 GEMM blocks,
+    the heavy-first triangular products and the one-panel look-ahead of the
+    trailing updates (factors of 8192 and more), with partial 512-column
+    panels and partial blocks: A 9000 x 9000, B 8300 x 8300.  The Cholesky
+    factor of the AR(1) matrix is dense, so every trailing update carries
+    nonzero data, and the inverse must cancel to the bidiagonal L."""
+    import torch
+    dev = torch.device("cuda:0")
+
+    def ar1(d):
+        i = torch.arange(d, device=dev, dtype=torch.float32)
+        return 0.5 ** (i[:, None] - i[None, :]).abs()
+
+    import paper_2608_06291_amd as pk
+    log("case factor AR(1) closed form, A 9000, B 8300")
+    f = pk.factor(ar1(9000), ar1(8300), 0.0)
+    for which, d in (("A", 9000), ("B", 8300)):
+        L = f.export(which)
+        ref = torch.eye(d, device=dev, dtype=torch.float32)
+        idx = torch.arange(1, d, device=dev)
+        ref[idx, idx - 1] = -0.5
+        err = float((L - ref).abs().max())
+        log(f"[factor] AR(1) {which} d={d} max err {err:.3e}")
+        assert err <= 1e-6
+        del L, ref
+    f.close()
+
+
 def test_factor_identity_B_and_export_errors():
     import paper_2608_06291_amd as pk
     f = _factor(workloads.ar1_toeplitz(40, 0.5), None, 0.01)
