@@ -13,14 +13,16 @@
 #include <mutex>
 #include <set>
 #include <new>
+#include <functional>
 #include <string>
 #include <tuple>
 #include <vector>
 
 namespace bk {
-hipError_t factor_one(hipStream_t s, hipStream_t s2, hipEvent_t ev_panel, hipEvent_t ev_rest,
-                      const float* X, int64_t d, double lam, double* Z, double* Ninv, double* T,
-                      double* mean, int* fail, int64_t* fail_pivot, float* packed, int64_t nt);
+using FactorOp = std::function<hipError_t()>;
+void factor_ops(std::vector<FactorOp>& ops, hipStream_t s, hipStream_t s2, hipEvent_t ev_panel,
+                hipEvent_t ev_rest, const float* X, int64_t d, double lam, double* Z, double* Ninv,
+                double* T, double* mean, int* fail, int64_t* fail_pivot, float* packed, int64_t nt);
 hipError_t pack_identity(hipStream_t s, int64_t nt, float* packed);
 hipError_t unpack_factor(hipStream_t s, const float* packed, int64_t d, float* dst);
 
@@ -416,13 +418,20 @@ extern "C" bakron_status bakron_factor(const float* A, int64_t n, const float* B
         const int64_t mtB = cdiv(m, bk::TS);
         f->LB_tiles = mtB;
         e = hipMalloc(&f->LB, sizeof(float) * (size_t)(mtB * (mtB + 1) / 2) * bk::TILE_ELEMS);
-        if (e == hipSuccess)
-            e = bk::factor_one(sB, s2[1], evp[1], evr[1], B, m, (double)damp, Z[1], Ninv[1], T[1],
-                               scal + 1, flags + 1, reinterpret_cast<int64_t*>(flags) + 3, f->LB, mtB);
     }
+    // the two factorisations' enqueue steps, interleaved so that both streams
+    // start at once
+    std::vector<bk::FactorOp> opsA, opsB;
+    if (e == hipSuccess && B)
+        bk::factor_ops(opsB, sB, s2[1], evp[1], evr[1], B, m, (double)damp, Z[1], Ninv[1], T[1],
+                       scal + 1, flags + 1, reinterpret_cast<int64_t*>(flags) + 3, f->LB, f->LB_tiles);
     if (e == hipSuccess)
-        e = bk::factor_one(stream, s2[0], evp[0], evr[0], A, n, (double)damp, Z[0], Ninv[0], T[0],
-                           scal, flags, reinterpret_cast<int64_t*>(flags) + 2, f->LA, ntA);
+        bk::factor_ops(opsA, stream, s2[0], evp[0], evr[0], A, n, (double)damp, Z[0], Ninv[0], T[0],
+                       scal, flags, reinterpret_cast<int64_t*>(flags) + 2, f->LA, ntA);
+    for (size_t i = 0; e == hipSuccess && (i < opsA.size() || i < opsB.size()); ++i) {
+        if (i < opsB.size()) e = opsB[i]();
+        if (e == hipSuccess && i < opsA.size()) e = opsA[i]();
+    }
     if (e == hipSuccess && B) {
         e = hipEventRecord(ev[1], sB);
         if (e == hipSuccess) e = hipStreamWaitEvent(stream, ev[1], 0);

@@ -15,7 +15,13 @@
 // fp32 and stored as packed lower-triangular TS x TS tiles for the solver.
 #include "common.h"
 
+#include <functional>
+
 namespace bk {
+
+// One enqueue step of a factorisation: a few launches (or event records and
+// waits) in stream order.
+using FactorOp = std::function<hipError_t()>;
 
 constexpr int NB = 64;  // factor block
 constexpr int NB2 = 512;  // Cholesky panel (multiple of NB)
@@ -416,38 +422,43 @@ static hipError_t gemm_f64(hipStream_t s, int64_t M, int64_t N, int64_t K, doubl
 }
 
 // Recursive lower-triangular inverse: Ninv[off:off+sz, off:off+sz] from C.
-// Diagonal NB-blocks must already be inverted.
-static hipError_t trtri_rec(hipStream_t s, const double* C, double* Ninv, int64_t ld, int64_t off,
-                            int64_t sz, double* T, const int* fail) {
-    if (sz <= NB) return hipSuccess;
+// Diagonal NB-blocks must already be inverted.  Appends its launches to ops.
+static void trtri_ops(std::vector<FactorOp>& ops, hipStream_t s, const double* C, double* Ninv,
+                      int64_t ld, int64_t off, int64_t sz, double* T, const int* fail) {
+    if (sz <= NB) return;
     int64_t nblk = (sz + NB - 1) / NB;
     int64_t h = ((nblk + 1) / 2) * NB;
     if (h >= sz) h = sz - NB;
-    hipError_t e = trtri_rec(s, C, Ninv, ld, off, h, T, fail);
-    if (e != hipSuccess) return e;
-    e = trtri_rec(s, C, Ninv, ld, off + h, sz - h, T, fail);
-    if (e != hipSuccess) return e;
+    trtri_ops(ops, s, C, Ninv, ld, off, h, T, fail);
+    trtri_ops(ops, s, C, Ninv, ld, off + h, sz - h, T, fail);
     const int64_t n2 = sz - h;
-    // T (n2 x h) = C21 * N11 (N11 lower triangular)
-    e = gemm_f64(s, n2, h, h, 1.0, C + (off + h) * ld + off, ld, Ninv + off * ld + off, ld, 0, 0.0, T,
-               h, 0, fail, 2);
-    if (e != hipSuccess) return e;
-    // N21 = -N22 * T (N22 lower triangular)
-    return gemm_f64(s, n2, h, n2, -1.0, Ninv + (off + h) * ld + (off + h), ld, T, h, 0, 0.0,
-                  Ninv + (off + h) * ld + off, ld, 0, fail, 1);
+    ops.push_back([=]() {
+        // T (n2 x h) = C21 * N11 (N11 lower triangular)
+        hipError_t e = gemm_f64(s, n2, h, h, 1.0, C + (off + h) * ld + off, ld, Ninv + off * ld + off,
+                                ld, 0, 0.0, T, h, 0, fail, 2);
+        if (e != hipSuccess) return e;
+        // N21 = -N22 * T (N22 lower triangular)
+        return gemm_f64(s, n2, h, n2, -1.0, Ninv + (off + h) * ld + (off + h), ld, T, h, 0, 0.0,
+                        Ninv + (off + h) * ld + off, ld, 0, fail, 1);
+    });
 }
 
-// Factor one matrix.  Z, Ninv: d*d doubles; T: d*d/4 + d*NB doubles;
+// The factorisation of one matrix as a list of enqueue steps (a few launches
+// each, in stream order), so that the host can interleave the steps of two
+// factorisations on their two streams: enqueued one after the other, the
+// second stream would sit idle while the host issues the first one's
+// hundreds of launches.  Z, Ninv: d*d doubles; T: d*d/4 + d*NB doubles;
 // flag: 1 int + 1 int64 (fail, pivot) zeroed by the caller.  With s2 (and
 // its two events) the Cholesky looks one panel ahead; s2's work is ordered
-// before everything enqueued on s after the call.
-hipError_t factor_one(hipStream_t s, hipStream_t s2, hipEvent_t ev_panel, hipEvent_t ev_rest,
-                      const float* X, int64_t d, double lam, double* Z, double* Ninv, double* T,
-                      double* mean, int* fail, int64_t* fail_pivot, float* packed, int64_t nt) {
-    hipLaunchKernelGGL(k_diag_mean, dim3(1), dim3(256), 0, s, X, d, mean);
-    hipLaunchKernelGGL(k_flip_damp, dim3(grid1d(d * d)), dim3(256), 0, s, X, d, mean, lam, Z);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
+// before everything enqueued on s after the last step.
+void factor_ops(std::vector<FactorOp>& ops, hipStream_t s, hipStream_t s2, hipEvent_t ev_panel,
+                hipEvent_t ev_rest, const float* X, int64_t d, double lam, double* Z, double* Ninv,
+                double* T, double* mean, int* fail, int64_t* fail_pivot, float* packed, int64_t nt) {
+    ops.push_back([=]() {
+        hipLaunchKernelGGL(k_diag_mean, dim3(1), dim3(256), 0, s, X, d, mean);
+        hipLaunchKernelGGL(k_flip_damp, dim3(grid1d(d * d)), dim3(256), 0, s, X, d, mean, lam, Z);
+        return hipGetLastError();
+    });
     // Two-level right-looking Cholesky: panels of NB2 columns, each factored
     // in NB-column steps (diagonal block, substitution for every row below,
     // update of the panel's remaining columns), then one rank-NB2 update of
@@ -463,17 +474,18 @@ hipError_t factor_one(hipStream_t s, hipStream_t s2, hipEvent_t ev_panel, hipEve
         const int64_t pend = (d - p0) < NB2 ? d : p0 + NB2;
         for (int64_t k0 = p0; k0 < pend; k0 += NB) {
             const int b = (int)((pend - k0) < NB ? (pend - k0) : NB);
-            hipLaunchKernelGGL(k_potrf_diag, dim3(1), dim3(NB), 0, s, Z, d, k0, b, fail, fail_pivot);
-            const int64_t rest = d - k0 - b;
-            if (rest > 0) {
+            ops.push_back([=]() {
+                hipLaunchKernelGGL(k_potrf_diag, dim3(1), dim3(NB), 0, s, Z, d, k0, b, fail, fail_pivot);
+                const int64_t rest = d - k0 - b;
+                if (rest <= 0) return hipGetLastError();
                 // panel solve: P <- P C_kk^-T by substitution
                 hipLaunchKernelGGL(k_trsm_panel, dim3((unsigned)((rest + 255) / 256)), dim3(256), 0,
                                    s, Z, d, k0, b, rest, fail);
                 // the panel's remaining columns: Z[k0+b:, k0+b:pend] -= P P[k0+b:pend]^T
-                e = gemm_f64(s, rest, pend - k0 - b, b, -1.0, Z + (k0 + b) * d + k0, d,
-                             Z + (k0 + b) * d + k0, d, 1, 1.0, Z + (k0 + b) * d + (k0 + b), d, 1, fail);
-                if (e != hipSuccess) return e;
-            }
+                return gemm_f64(s, rest, pend - k0 - b, b, -1.0, Z + (k0 + b) * d + k0, d,
+                                Z + (k0 + b) * d + k0, d, 1, 1.0, Z + (k0 + b) * d + (k0 + b), d, 1,
+                                fail);
+            });
         }
         const int64_t rest = d - pend;
         if (rest <= 0) continue;
@@ -481,31 +493,41 @@ hipError_t factor_one(hipStream_t s, hipStream_t s2, hipEvent_t ev_panel, hipEve
         const int64_t kp = pend - p0;
         // split point: the end of the next panel (no split without s2)
         const int64_t nend = (s2 && d - pend > NB2) ? pend + NB2 : d;
-        if (nend < d) {   // Z[nend:, nend:] -= P P^T on s2, after this panel
-            if ((e = hipEventRecord(ev_panel, s)) != hipSuccess) return e;
-            if ((e = hipStreamWaitEvent(s2, ev_panel, 0)) != hipSuccess) return e;
-            e = gemm_f64(s2, d - nend, d - nend, kp, -1.0, P + (nend - pend) * d, d,
-                         P + (nend - pend) * d, d, 1, 1.0, Z + nend * d + nend, d, 1, fail);
+        const bool wait_prev = s2 && p0 > 0;
+        ops.push_back([=]() {
+            hipError_t e;
+            if (nend < d) {   // Z[nend:, nend:] -= P P^T on s2, after this panel
+                if ((e = hipEventRecord(ev_panel, s)) != hipSuccess) return e;
+                if ((e = hipStreamWaitEvent(s2, ev_panel, 0)) != hipSuccess) return e;
+                e = gemm_f64(s2, d - nend, d - nend, kp, -1.0, P + (nend - pend) * d, d,
+                             P + (nend - pend) * d, d, 1, 1.0, Z + nend * d + nend, d, 1, fail);
+                if (e != hipSuccess) return e;
+            }
+            // the previous panel's rest update also wrote these columns
+            if (wait_prev && (e = hipStreamWaitEvent(s, ev_rest, 0)) != hipSuccess) return e;
+            // Z[pend:, pend:nend] -= P P[pend:nend]^T on s
+            e = gemm_f64(s, rest, nend - pend, kp, -1.0, P, d, P, d, 1, 1.0, Z + pend * d + pend, d, 1,
+                         fail);
             if (e != hipSuccess) return e;
-        }
-        // the previous panel's rest update also wrote these columns
-        if (s2 && p0 > 0 && (e = hipStreamWaitEvent(s, ev_rest, 0)) != hipSuccess) return e;
-        // Z[pend:, pend:nend] -= P P[pend:nend]^T on s
-        e = gemm_f64(s, rest, nend - pend, kp, -1.0, P, d, P, d, 1, 1.0, Z + pend * d + pend, d, 1, fail);
-        if (e != hipSuccess) return e;
-        if (nend < d && (e = hipEventRecord(ev_rest, s2)) != hipSuccess) return e;
+            if (nend < d) e = hipEventRecord(ev_rest, s2);
+            return e;
+        });
     }
-    // Ninv = C^-1 (lower); upper part must be zero for the recursive GEMMs
-    e = hipMemsetAsync(Ninv, 0, sizeof(double) * d * d, s);
-    if (e != hipSuccess) return e;
-    const int64_t nblk = (d + NB - 1) / NB;
-    hipLaunchKernelGGL(k_inv_lower_blocks, dim3((unsigned)nblk), dim3(NB), 0, s, Z, d, Ninv, d,
-                       (int64_t)0, d, (int64_t)0, fail);
-    e = trtri_rec(s, Z, Ninv, d, 0, d, T, fail);
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(k_pack_factor, dim3(grid1d(nt * (nt + 1) / 2 * TILE_ELEMS)), dim3(256), 0, s,
-                       Z, Ninv, d, d, nt, packed);
-    return hipGetLastError();
+    ops.push_back([=]() {
+        // Ninv = C^-1 (lower); upper part must be zero for the recursive GEMMs
+        hipError_t e = hipMemsetAsync(Ninv, 0, sizeof(double) * d * d, s);
+        if (e != hipSuccess) return e;
+        const int64_t nblk = (d + NB - 1) / NB;
+        hipLaunchKernelGGL(k_inv_lower_blocks, dim3((unsigned)nblk), dim3(NB), 0, s, Z, d, Ninv, d,
+                           (int64_t)0, d, (int64_t)0, fail);
+        return hipGetLastError();
+    });
+    trtri_ops(ops, s, Z, Ninv, d, 0, d, T, fail);
+    ops.push_back([=]() {
+        hipLaunchKernelGGL(k_pack_factor, dim3(grid1d(nt * (nt + 1) / 2 * TILE_ELEMS)), dim3(256), 0,
+                           s, Z, Ninv, d, d, nt, packed);
+        return hipGetLastError();
+    });
 }
 
 hipError_t pack_identity(hipStream_t s, int64_t nt, float* packed) {

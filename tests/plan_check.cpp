@@ -6,6 +6,7 @@
 // never run while a main op writes the same tiles; the host enqueue order
 // respects every wait.  The launch functions are stubbed out: only the host
 // planning code runs.  Exit status = number of failing cases.
+#include <functional>
 #include "api.hip"
 #include <cstdio>
 #include <map>
@@ -130,7 +131,7 @@ int main() {
     return fails;
 }
 namespace bk {
-hipError_t factor_one(hipStream_t, hipStream_t, hipEvent_t, hipEvent_t, const float*, int64_t, double, double*, double*, double*, double*, int*, int64_t*, float*, int64_t) { return hipSuccess; }
+void factor_ops(std::vector<std::function<hipError_t()>>&, hipStream_t, hipStream_t, hipEvent_t, hipEvent_t, const float*, int64_t, double, double*, double*, double*, double*, int*, int64_t*, float*, int64_t) {}
 hipError_t pack_identity(hipStream_t, int64_t, float*) { return hipSuccess; }
 hipError_t unpack_factor(hipStream_t, const float*, int64_t, float*) { return hipSuccess; }
 int plan_timed_launches(const Plan&) { return 0; }
