@@ -96,7 +96,12 @@ typedef struct {
  *   m     > 0 when B != NULL
  *   damp  >= 0, finite: X <- X + damp * mean(diag X) * I, each matrix with
  *         its own mean diagonal (Sec. 4 opening; App. D)
- *   stream  HIP stream for all work (0 = default stream)
+ *   stream  HIP stream the work is ordered on (0 = default stream).  The
+ *         call also creates non-blocking streams of its own, forked from
+ *         and joined back into `stream`, and destroys them before it
+ *         returns: one for B (A and B are factored concurrently) and, for a
+ *         factor of 8192 or more, one that runs its trailing updates one
+ *         panel ahead
  *   out   receives the handle on BAKRON_OK; untouched otherwise
  *
  * Computes, in fp64 on the device, L^X = R_X^-1 diag(R_X) where
@@ -135,7 +140,8 @@ bakron_status bakron_factor(const float *A, int64_t n, const float *B, int64_t m
  * (BAKRON_DEFER unset), the first solve of that shape on the handle runs
  * both plans twice each, times them with events on `stream` (one host
  * synchronisation), keeps the faster for the handle and returns the outputs
- * of its last run.  On the legacy default stream, which
+ * of its last run (not while per-launch profiling is enabled, which keeps
+ * the model's choice).  On the legacy default stream, which
  * synchronises implicitly with such streams, and while `stream` is being
  * captured into a graph, everything runs on `stream`.  Unless
  * BAKRON_DEFER=0, the first solve planned on a device creates the two
