@@ -26,6 +26,30 @@ def test_parity_shapes(oracle_mod, m, n):
     check_against_oracle(p, codes, V, pre, oracle_mod, label=f"shape{m}x{n}")
 
 
+def _sweep_cases(count=24):
+    """Seeded random cases: shape (ragged in both directions, up to 200 x 200),
+    alphabet size, near-field distance and B = I."""
+    rng = np.random.Generator(np.random.PCG64(20261202))
+    cases = []
+    for _ in range(count):
+        m, n = (int(x) for x in rng.integers(1, 201, size=2))
+        bits = int(rng.choice([2, 3, 4, 8]))
+        k = [None, 0, 2, 5, 8][int(rng.integers(0, 5))]
+        ident = bool(rng.random() < 0.2)
+        cases.append((m, n, bits, k, ident, int(rng.integers(0, 1 << 30))))
+    return cases
+
+
+@pytest.mark.parametrize("m,n,bits,k,ident,seed", _sweep_cases())
+def test_parity_random_sweep(oracle_mod, m, n, bits, k, ident, seed):
+    """Element-wise tie-forced parity on a seeded random sweep of shapes,
+    alphabets, near-field distances and one-sided (B = I) problems."""
+    p = workloads.make_random(m, n, seed, bits=bits, identity_B=ident)
+    log(f"case sweep m={m} n={n} bits={bits} knear={k} identity_B={ident} seed={seed}")
+    codes, V, pre = gpu_run(p, k=k)
+    check_against_oracle(p, codes, V, pre, oracle_mod, label=f"sweep{m}x{n}b{bits}k{k}i{int(ident)}")
+
+
 @pytest.mark.parametrize("k", [0, 1, 3, 8])
 @pytest.mark.parametrize("m,n", [(200, 300), (300, 200), (161, 161)])
 def test_parity_node_paths(oracle_mod, m, n, k):
