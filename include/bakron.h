@@ -151,16 +151,20 @@ bakron_status bakron_factor(const float *A, int64_t n, const float *B, int64_t m
  * BAKRON_EHIP on a later call or at the caller's synchronisation.
  *
  * With B = NULL at bakron_factor (B = I) the rows are independent and the
- * solve is Alg. 1 on every row (GPTQ with Hessian A, Sec. 1): one launch on
- * `stream`, one workgroup per 16 rows walking the columns in blocks of 32
- * with the feedback of earlier blocks applied lazily; its workspace is
- * 4 * ceil(m/16)*16 * ceil(n/32)*32 + 256 bytes, allocated on the first call
+ * solve is Alg. 1 on every row (GPTQ with Hessian A, Sec. 1), all on
+ * `stream`: the columns are taken in ranges of 1024; per range one launch
+ * rounds it (one workgroup per 16 rows, blocks of 32 columns, the feedback
+ * of the range's earlier blocks applied lazily) and one launch pushes its
+ * errors into every later column of a working copy of W.  Its workspace is
+ * 8 * ceil(m/16)*16 * ceil(n/32)*32 + 256 bytes, allocated on the first call
  * for a shape.  The environment variable BAKRON_GPTQ=0 at handle creation sends
  * such solves through the two-sided solver instead (same codes up to fp32
  * summation order).  Debug switches read at handle creation:
  * BAKRON_KNEAR=k (0..8) sets how many tile anti-diagonals a tile pulls from
  * itself instead of receiving them from node pushes; BAKRON_MACRO=4 or 2
- * forces 128 x 128 or 64 x 64 macro tiles in every node push.
+ * forces 128 x 128 or 64 x 64 macro tiles in every node push;
+ * BAKRON_GPTQ_RANGE=t (1..64) sets the one-sided range to t column tiles of
+ * 32 (the tests use it to run several ranges on small shapes).
  */
 bakron_status bakron_solve(const float *W, int64_t m, int64_t n, const bakron_factors *f,
                            bakron_quantizer q, int8_t *codes, float *V, hipStream_t stream);

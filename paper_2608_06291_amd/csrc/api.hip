@@ -38,7 +38,7 @@ hipError_t run_antidiag(hipStream_t st, const float* W, int64_t m, int64_t n, fl
                         int8_t* codes, float* V, float* pre);
 size_t gptq_workspace_floats(int64_t m, int64_t n);
 hipError_t run_gptq(hipStream_t st, const float* W, int64_t m, int64_t n, const float* LA, float* E,
-                    const QuantArgs& q, int8_t* codes, float* V, float* pre);
+                    const QuantArgs& q, int8_t* codes, float* V, float* pre, int range_tiles);
 }  // namespace bk
 
 struct bakron_factors {
@@ -92,6 +92,7 @@ struct bakron_factors {
     // one int for the debug scale check); BAKRON_GPTQ=0 at creation sends
     // B = I solves through the two-sided solver instead
     int gptq = 1;
+    int gptq_range = 0;   // column tiles per one-sided range (0: the library's default)
     int64_t gq_m = -1, gq_n = -1;
     float* gq_mem = nullptr;
     // BaKron-antidiagonal working copy of W and one diagonal's errors
@@ -348,6 +349,10 @@ extern "C" bakron_status bakron_factor(const float* A, int64_t n, const float* B
         if (v >= 0 && v <= bk::KNEAR_MAX) f->knear = v;
     }
     if (const char* gq = std::getenv("BAKRON_GPTQ")) f->gptq = std::atoi(gq) != 0;
+    if (const char* gr = std::getenv("BAKRON_GPTQ_RANGE")) {
+        const int v = std::atoi(gr);
+        if (v >= 1 && v <= 64) f->gptq_range = v;
+    }
     if (const char* mc = std::getenv("BAKRON_MACRO")) {
         int v = std::atoi(mc);
         if (v == 2 || v == 4) f->macro = v;
@@ -841,7 +846,7 @@ static bakron_status debug_scale_check(bakron_factors* f, const bakron_quantizer
     return BAKRON_OK;
 }
 
-// B = I: the rows are independent (GPTQ with Hessian A on every row); one launch
+// B = I: the rows are independent (GPTQ with Hessian A on every row)
 static bakron_status solve_gptq(bakron_factors* f, const float* W, int64_t m, int64_t n,
                                 const bakron_quantizer& q, int8_t* codes, float* V, float* pre,
                                 hipStream_t stream) {
@@ -862,7 +867,7 @@ static bakron_status solve_gptq(bakron_factors* f, const float* W, int64_t m, in
     }
     hipError_t e = hipSuccess;
     if (f->poison) e = bk::fill_words(stream, f->gq_mem, (int64_t)ef, 0xFFFFFFFFu);
-    if (e == hipSuccess) e = bk::run_gptq(stream, W, m, n, f->LA, f->gq_mem, qa, codes, V, pre);
+    if (e == hipSuccess) e = bk::run_gptq(stream, W, m, n, f->LA, f->gq_mem, qa, codes, V, pre, f->gptq_range);
     if (e != hipSuccess) return hip_fail(&f->err, e, "bakron_solve: launch (one-sided)");
     f->prof_valid = 0;   // the per-launch measurement hook covers the two-sided solver only
     return BAKRON_OK;

@@ -138,7 +138,7 @@ int plan_timed_launches(const Plan&) { return 0; }
 hipError_t fill_words(hipStream_t, void*, int64_t, uint32_t) { return hipSuccess; }
 hipError_t check_scales(hipStream_t, const float*, int64_t, int*) { return hipSuccess; }
 size_t gptq_workspace_floats(int64_t, int64_t) { return 0; }
-hipError_t run_gptq(hipStream_t, const float*, int64_t, int64_t, const float*, float*, const QuantArgs&, int8_t*, float*, float*) { return hipSuccess; }
+hipError_t run_gptq(hipStream_t, const float*, int64_t, int64_t, const float*, float*, const QuantArgs&, int8_t*, float*, float*, int) { return hipSuccess; }
 hipError_t run_plan(hipStream_t, hipStream_t, const Plan&, const float*, int64_t, int64_t, int, int, const Workspace&, const float*, const float*, int, const QuantArgs&, int8_t*, float*, float*, int, int, const int4*, hipEvent_t*, hipEvent_t*, hipEvent_t*) { return hipSuccess; }
 hipError_t run_antidiag(hipStream_t, const float*, int64_t, int64_t, float*, float*, const float*, const float*, const QuantArgs&, int8_t*, float*, float*) { return hipSuccess; }
 }

@@ -44,6 +44,19 @@ def test_gptq_shapes(oracle_mod, m, n):
     check_against_oracle(p, codes, V, pre, oracle_mod, label=f"gptq{m}x{n}")
 
 
+@pytest.mark.parametrize("rng_tiles,m,n", [(1, 65, 97), (3, 130, 257), (2, 257, 97), (5, 200, 300),
+                                             (1, 16, 70)])
+def test_gptq_multi_range(oracle_mod, rng_tiles, m, n):
+    """Column ranges of a few tiles (BAKRON_GPTQ_RANGE), so that small ragged
+    shapes run several ranges and the pushes between them (partial last
+    range, partial row and column blocks of the push)."""
+    p = _problem(m, n, seed=900 + rng_tiles + m + 3 * n)
+    log(f"case one-sided m={m} n={n} range={rng_tiles} tiles")
+    with _env(BAKRON_GPTQ_RANGE=rng_tiles):
+        codes, V, pre = gpu_run(p)
+    check_against_oracle(p, codes, V, pre, oracle_mod, label=f"gptq{m}x{n}r{rng_tiles}")
+
+
 @pytest.mark.parametrize("variant", ["bits2", "bits8", "asym+groups+cols", "zero-rows"])
 def test_gptq_quantisers(oracle_mod, variant):
     m, n = 90, 150
@@ -85,11 +98,17 @@ def test_gptq_large_with_recursive_oracle(oracle_mod):
     check_against_oracle(p, codes, V, pre, oracle_mod, label="gptq-1000x2080", method="recursive")
 
 
-def test_gptq_deterministic_and_poison_free():
+@pytest.mark.parametrize("rng_tiles", [None, 2])
+def test_gptq_deterministic_and_poison_free(rng_tiles):
+    """Repeated solves are bitwise equal, and so is a solve whose workspace
+    (errors and the working copy of W) was filled with NaN first: nothing is
+    read before it is written, also across ranges (2-tile ranges)."""
     p = _problem(150, 230, seed=64)
-    log("case one-sided determinism and poisoned workspace")
-    (c1, v1, x1), (c2, v2, x2) = gpu_run(p, repeat=2)
-    with _env(BAKRON_POISON=1):
+    log(f"case one-sided determinism and poisoned workspace, range {rng_tiles}")
+    env = {} if rng_tiles is None else {"BAKRON_GPTQ_RANGE": rng_tiles}
+    with _env(**env):
+        (c1, v1, x1), (c2, v2, x2) = gpu_run(p, repeat=2)
+    with _env(BAKRON_POISON=1, **env):
         c3, v3, x3 = gpu_run(p)
     for c, v, x in ((c2, v2, x2), (c3, v3, x3)):
         assert np.array_equal(c1, c)
