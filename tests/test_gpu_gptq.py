@@ -57,8 +57,9 @@ def test_gptq_multi_range(oracle_mod, rng_tiles, m, n):
     check_against_oracle(p, codes, V, pre, oracle_mod, label=f"gptq{m}x{n}r{rng_tiles}")
 
 
+@pytest.mark.parametrize("rng_tiles", [None, 2])
 @pytest.mark.parametrize("variant", ["bits2", "bits8", "asym+groups+cols", "zero-rows"])
-def test_gptq_quantisers(oracle_mod, variant):
+def test_gptq_quantisers(oracle_mod, variant, rng_tiles):
     m, n = 90, 150
     p = _problem(m, n, seed=61, bits={"bits2": 2, "bits8": 8}.get(variant, 4))
     if variant == "asym+groups+cols":
@@ -71,9 +72,11 @@ def test_gptq_quantisers(oracle_mod, variant):
     if variant == "zero-rows":
         p["scale"] = p["scale"].copy()
         p["scale"][[0, 45, 89]] = 0.0
-    log(f"case one-sided quantiser {variant}")
-    codes, V, pre = gpu_run(p)
-    check_against_oracle(p, codes, V, pre, oracle_mod, label=f"gptq-{variant}")
+    log(f"case one-sided quantiser {variant}, range {rng_tiles}")
+    env = {} if rng_tiles is None else {"BAKRON_GPTQ_RANGE": rng_tiles}
+    with _env(**env):
+        codes, V, pre = gpu_run(p)
+    check_against_oracle(p, codes, V, pre, oracle_mod, label=f"gptq-{variant}-r{rng_tiles}")
 
 
 def test_gptq_against_two_sided_solver(oracle_mod):
