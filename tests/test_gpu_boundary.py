@@ -101,3 +101,49 @@ def test_give_up_record_is_sticky_until_checked(oracle_mod):
     check_against_oracle(p, codes.cpu().numpy(), V.cpu().numpy(), pre.cpu().numpy(), oracle_mod,
                          label="after-check")
     f.close()
+
+
+def test_two_handles_on_two_streams_bitwise():
+    """Two handles (two shapes) solved on two user streams, their solves
+    enqueued back to back with no synchronisation in between: both share the
+    device's CU-restricted streams and the process-wide plan cache, and each
+    result is bitwise the same as the handle's solve alone."""
+    import torch
+    import paper_2608_06291_amd as pk
+    from gpu_util import gpu_run
+    dev = torch.device("cuda:0")
+    cases = [(1024, 1024, 11), (700, 900, 12)]
+    probs = [workloads.make_random(m, n, seed=s) for m, n, s in cases]
+    log("case two handles on two streams: references")
+    refs = [gpu_run(p) for p in probs]
+    hs, outs, ins = [], [], []
+    streams = [torch.cuda.Stream(dev) for _ in cases]
+    for p, st in zip(probs, streams):
+        with torch.cuda.stream(st):
+            A = torch.from_numpy(p["A"]).to(dev)
+            B = torch.from_numpy(p["B"]).to(dev)
+            W = torch.from_numpy(p["W"]).to(dev)
+            s = torch.from_numpy(p["scale"]).to(dev)
+            f = pk.factor(A, B, p["damp"])
+            m, n = W.shape
+            o = (torch.full((m, n), 100, dtype=torch.int8, device=dev),
+                 torch.full((m, n), float("nan"), dtype=torch.float32, device=dev),
+                 torch.full((m, n), float("nan"), dtype=torch.float32, device=dev))
+            pk.solve(W, f, p["bits"], s, codes=o[0], V=o[1], pre=o[2], debug=True)   # first solve of the shape
+        hs.append(f)
+        outs.append(o)
+        ins.append((W, s, p["bits"]))
+    torch.cuda.synchronize()
+    log("case two handles on two streams: interleaved solves")
+    for _ in range(3):
+        for f, o, (W, s, bits), st in zip(hs, outs, ins, streams):
+            with torch.cuda.stream(st):
+                pk.solve(W, f, bits, s, codes=o[0], V=o[1], pre=o[2], debug=True)
+    torch.cuda.synchronize()
+    for f, o, (c0, v0, x0) in zip(hs, outs, refs):
+        assert f.check()
+        c, v, x = (t.cpu().numpy() for t in o)
+        assert np.array_equal(c, c0)
+        assert np.array_equal(v.view(np.uint32), v0.view(np.uint32))
+        assert np.array_equal(np.nan_to_num(x).view(np.uint32), np.nan_to_num(x0).view(np.uint32))
+        f.close()
