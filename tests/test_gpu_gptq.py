@@ -143,3 +143,33 @@ def test_gptq_certificate_wide_table3_shape(oracle_mod):
     assert v["violations"] == 0
     assert v["flips"] <= 1e-4 * m * n
     assert margin < 1e-4
+
+
+def test_gptq_handle_alternating_row_counts():
+    """With B = NULL the row count is free per call: one handle solving
+    300, 130 and again 300 rows (the workspace is reallocated at each change
+    of shape) gives bitwise the results of a fresh handle per shape."""
+    import torch
+    import paper_2608_06291_amd as pk
+    dev = torch.device("cuda:0")
+    n = 230
+    p300 = _problem(300, n, seed=71)
+    p130 = _problem(130, n, seed=72)
+    p130["A"] = p300["A"]                 # one factor A for both row counts
+    refs = {}
+    for key, p in (("300", p300), ("130", p130)):
+        refs[key] = gpu_run(p)
+    log("case one-sided handle with alternating row counts")
+    f = pk.factor(torch.from_numpy(p300["A"]).to(dev), None, p300["damp"])
+    for key, p in (("300", p300), ("130", p130), ("300", p300)):
+        W = torch.from_numpy(p["W"]).to(dev)
+        s = torch.from_numpy(p["scale"]).to(dev)
+        c, v, x = pk.solve(W, f, p["bits"], s, debug=True)
+        torch.cuda.synchronize()
+        assert f.check()
+        c0, v0, x0 = refs[key]
+        assert np.array_equal(c.cpu().numpy(), c0)
+        assert np.array_equal(v.cpu().numpy().view(np.uint32), v0.view(np.uint32))
+        assert np.array_equal(np.nan_to_num(x.cpu().numpy()).view(np.uint32),
+                              np.nan_to_num(x0).view(np.uint32))
+    f.close()
